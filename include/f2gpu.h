@@ -1,0 +1,162 @@
+/*
+ * f2gpu.h -- C ABI of the MI355X (gfx950) GF(2) affine-map learner.
+ *
+ * Method: F2Asm, "Learning Exact NVIDIA SASS Encoders with F2 Linear Algebra".
+ *   Fitting solves, for every encoding context, the training system Phi W = Y
+ *   over GF(2) (Sec. 2.1, Eq. 3) by streaming Gaussian elimination on
+ *   augmented rows [phi | y] (Sec. 2.2, Eq. 5): each row is reduced against
+ *   the retained pivot basis, a zero-feature residual with a nonzero output
+ *   is a contradiction (Eq. 8), otherwise its highest-priority feature bit
+ *   becomes a new pivot, that pivot is cleared from the stored rows and the
+ *   row is inserted.  Encoding reduces a query phi(x) by the stored rows and
+ *   XORs their outputs; a nonzero residual proves the query lies outside the
+ *   observed span S = rowspan(Phi) (Sec. 2.3, Eqs. 6-9).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every pointer argument is DEVICE memory allocated and owned by the
+ *    caller unless its name ends in _host.  The library allocates nothing and
+ *    keeps no state between calls; concurrent calls need distinct workspaces.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *    device work is enqueued on it; outputs are valid once it has synchronised.
+ *  - A negative return value means nothing was enqueued (argument errors that
+ *    the host can check, or a HIP launch failure).  Data conditions found on
+ *    the device (contradictions, unsupported queries, malformed segments, bad
+ *    context ids) are never errors: they are reported per context or per query.
+ *
+ * Row layout of a context with input width n (d = n + 1 features)
+ * -----------------------------------------------------------------
+ *  fw = ceil(d / 64) little-endian uint64 feature words, then 2 output words:
+ *    storage bit i < n  : input bit x_i
+ *    storage bit n      : the constant feature (the leading 1 of Eq. 1); it is
+ *                         taken from the row as given, so linear systems such
+ *                         as the worked example of App. B can be expressed
+ *    bits above n       : padding, ignored
+ *    word fw, fw + 1    : output y, bits 0-63 then 64-127 (a 128-bit word)
+ *  Pivot priority follows the feature index of Eq. 1: the constant has index
+ *  0 and x_i has index i + 1, so x_{n-1} has the highest priority and the
+ *  constant the lowest.  A pivot is reported as its storage bit index.
+ */
+#ifndef F2GPU_H
+#define F2GPU_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    F2_OK = 0,
+    F2_EINVAL = -1,      /* null pointer, negative count, bad stride, ... */
+    F2_EWORKSPACE = -2,  /* workspace missing or smaller than required */
+    F2_EDEVICE = -3,     /* HIP error while enqueuing */
+    F2_ETOOWIDE = -4     /* host-side layout helper: a width above F2_MAX_N_BITS */
+} f2_status;
+
+#define F2_MAX_N_BITS 4095 /* widest supported context: fw <= 64 feature words */
+#define F2_Y_WORDS 2       /* the 128-bit output word */
+
+/* per-context flags (ctx_flags) */
+enum {
+    F2_CTX_CONTRADICTION = 1u, /* n_contra > 0: some row had a zero-feature, nonzero-output residual */
+    F2_CTX_BAD_SEGMENT = 2u,   /* row segment negative, past rows_words, or not a multiple of fw+2 words */
+    F2_CTX_BAD_WIDTH = 4u,     /* n_bits outside [0, F2_MAX_N_BITS] */
+    F2_CTX_BAD_OUTPUT = 8u     /* output offsets of this context fall outside the output buffers */
+};
+
+/* per-query flags (qflags_out) */
+enum {
+    F2_Q_OUT_OF_SPAN = 1u,       /* phi(x) is not in the observed span: word is 0 */
+    F2_Q_CTX_CONTRADICTORY = 2u, /* the context's training data held a contradiction */
+    F2_Q_BAD_CTX = 4u            /* context id out of range or context not fitted: word is 0 */
+};
+
+/*
+ * Fit outputs, and the model that encoding reads.  A host struct holding
+ * device pointers.  Per context c:
+ *   basis[basis_off[c] ...]   rank[c] rows of fw+2 words in descending pivot
+ *                             priority (capacity (n+1)(fw+2) words; rows past
+ *                             the rank are scratch, their content unspecified)
+ *   pivots[piv_off[c] ...]    rank[c] storage bit indices, same order
+ *                             (capacity n+1 entries)
+ *   maps[map_off[c] ...]      the canonical dense map: n+1 columns of 2 words,
+ *                             column j = storage bit j; column p = z_p for every
+ *                             pivot p and 0 for every other column (one linear
+ *                             extension of T beyond the span, Sec. 2.3)
+ *   rank[c], ctx_flags[c], n_contra[c] (rows flagged contradictory),
+ *   first_contra_row[c] (index within the context's segment, -1 if none).
+ * For a contradictory context the stored map is defined by the rows kept in
+ * stream order (each row independent of all earlier rows), which is what the
+ * streaming elimination retains.
+ */
+typedef struct f2_model {
+    int32_t num_ctx;
+    const int32_t* n_bits;    /* [num_ctx] input width n of each context */
+    const int64_t* basis_off; /* [num_ctx+1] uint64-word offsets into basis */
+    const int64_t* piv_off;   /* [num_ctx+1] int32-entry offsets into pivots */
+    const int64_t* map_off;   /* [num_ctx+1] uint64-word offsets into maps */
+    int64_t basis_words;      /* size of basis in uint64 words */
+    int64_t piv_entries;      /* size of pivots in int32 entries */
+    int64_t map_words;        /* size of maps in uint64 words */
+    uint64_t* basis;
+    int32_t* pivots;
+    uint64_t* maps;
+    int32_t* rank;            /* [num_ctx] */
+    uint32_t* ctx_flags;      /* [num_ctx] */
+    int32_t* n_contra;        /* [num_ctx] */
+    int64_t* first_contra_row;/* [num_ctx] */
+} f2_model;
+
+/*
+ * Host helper: output offsets for a batch (num_ctx+1 entries each, caller-
+ * allocated host arrays), packed in context order with the capacities above.
+ * Returns F2_OK, F2_EINVAL (null pointer, num_ctx < 0) or F2_ETOOWIDE.
+ */
+int f2_fit_layout(const int32_t* n_bits_host, int32_t num_ctx, int64_t* basis_off_host, int64_t* piv_off_host,
+                  int64_t* map_off_host);
+
+/* Workspace bytes f2_fit_batch needs for num_ctx contexts (any widths). */
+size_t f2_fit_workspace_bytes(int32_t num_ctx);
+
+/*
+ * Fit every context of a batch (Sec. 2.2).
+ *   rows      [rows_words] packed rows (layout above); context c owns the words
+ *             rows[row_off[c] .. row_off[c+1]), i.e. (row_off[c+1]-row_off[c])/(fw+2)
+ *             rows, processed in stream order
+ *   row_off   [num_ctx+1] uint64-word offsets
+ *   model     outputs; model->num_ctx contexts, model->n_bits their widths
+ *   workspace at least f2_fit_workspace_bytes(num_ctx) bytes, 256-byte aligned
+ * Returns F2_OK, F2_EINVAL, F2_EWORKSPACE or F2_EDEVICE.  Contexts are
+ * independent; results do not depend on launch geometry.
+ */
+int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* model_host,
+                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes f2_encode_batch needs for a fitted model (encode tables mirror the basis capacity). */
+size_t f2_encode_workspace_bytes(const f2_model* model_host);
+
+/*
+ * Encode a batch of queries against a fitted model (Sec. 2.3).
+ *   ctx_id     [num_queries] context of each query
+ *   x          [num_queries * x_stride_words] input bits x_0.. of each query,
+ *              little-endian; bits past the stride count as 0.  The feature
+ *              vector is phi = [x | 1] (Eq. 1): the constant is always 1.
+ *   words_out  [2 * num_queries] the 128-bit word T(phi) (0 when unsupported)
+ *   qflags_out [num_queries] F2_Q_* flags
+ * A query with any x bit at or above its context's width n lies outside that
+ * context's ambient space and is reported unsupported.
+ * Returns F2_OK, F2_EINVAL, F2_EWORKSPACE or F2_EDEVICE.
+ */
+int f2_encode_batch(const f2_model* model_host, const int32_t* ctx_id, const uint64_t* x, int32_t x_stride_words,
+                    int64_t num_queries, uint64_t* words_out, uint8_t* qflags_out, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* f2_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* F2GPU_H */

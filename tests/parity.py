@@ -1,0 +1,76 @@
+"""Helpers shared by the GPU parity tests: run the HIP library and the CPU
+oracle on the same seeded inputs and compare every output element by element
+(all outputs are bits or integers, so the bar is bit-exact equality)."""
+import numpy as np
+
+import oracle
+
+
+def to_dev(a, dtype=None):
+    import torch
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint64:
+        a = a.view(np.int64)
+    t = torch.from_numpy(a)
+    return t.to("cuda")
+
+
+def host(t, np_dtype):
+    return t.detach().cpu().numpy().view(np_dtype)
+
+
+def gpu_fit(f2, rows, row_off, n_bits):
+    import torch
+    model = f2.fit(to_dev(rows if rows.size else np.zeros(1, np.uint64)), to_dev(row_off), n_bits)
+    torch.cuda.synchronize()
+    return model
+
+
+def model_to_host(model):
+    return dict(
+        basis=host(model.basis, np.uint64), pivots=host(model.pivots, np.int32), maps=host(model.maps, np.uint64),
+        rank=host(model.rank, np.int32)[:model.num_ctx], flags=host(model.ctx_flags, np.uint32)[:model.num_ctx],
+        n_contra=host(model.n_contra, np.int32)[:model.num_ctx],
+        first=host(model.first_contra_row, np.int64)[:model.num_ctx])
+
+
+def compare_fit(model, ref: "oracle.FitResult", ctx=None):
+    """Bit-exact comparison of every defined output; returns the number of contexts checked."""
+    g = model_to_host(model)
+    C = model.num_ctx
+    assert np.array_equal(g["flags"], ref.flags[:C]), "ctx_flags"
+    assert np.array_equal(g["rank"], ref.rank[:C]), "rank"
+    assert np.array_equal(g["n_contra"], ref.n_contra[:C]), "n_contra"
+    assert np.array_equal(g["first"], ref.first_contra[:C]), "first_contra_row"
+    # layouts agree (same documented capacities)
+    assert np.array_equal(model.basis_off_host, ref.basis_off)
+    assert np.array_equal(model.piv_off_host, ref.piv_off)
+    assert np.array_equal(model.map_off_host, ref.map_off)
+    n = np.clip(ref.n_bits[:C].astype(np.int64), 0, oracle.MAX_N)
+    W = (n + 64) // 64 + 2
+    ok_ctx = (ref.flags[:C] & (oracle.CTX_BAD_WIDTH | oracle.CTX_BAD_OUTPUT)) == 0
+    # pivots [0, rank) and basis rows [0, rank) of every context
+    pmask = np.zeros(len(ref.pivots), bool)
+    bmask = np.zeros(len(ref.basis), bool)
+    mmask = np.zeros(len(ref.maps), bool)
+    r = ref.rank[:C].astype(np.int64)
+    for arr, off, length in ((pmask, ref.piv_off, r), (bmask, ref.basis_off, r * W), (mmask, ref.map_off, 2 * (n + 1))):
+        length = np.where(ok_ctx, length, 0)
+        starts = off[:C]
+        idx = np.repeat(starts - np.concatenate([[0], np.cumsum(length)[:-1]]), length) + np.arange(length.sum())
+        arr[idx] = True
+    assert np.array_equal(g["pivots"][:len(pmask)][pmask], ref.pivots[pmask]), "pivots"
+    bad = np.nonzero(g["basis"][:len(bmask)][bmask] != ref.basis[bmask])[0]
+    assert len(bad) == 0, f"basis mismatch at {len(bad)} words"
+    assert np.array_equal(g["maps"][:len(mmask)][mmask], ref.maps[mmask]), "maps"
+    return C
+
+
+def compare_encode(words_dev, qf_dev, ref_words, ref_qf, sample=None):
+    w = host(words_dev, np.uint64).reshape(-1, 2)
+    q = host(qf_dev, np.uint8)
+    if sample is not None:
+        w, q = w[sample], q[sample]
+    assert np.array_equal(q, ref_qf), f"qflags differ at {np.count_nonzero(q != ref_qf)} queries"
+    bad = np.nonzero((w != ref_words).any(axis=1))[0]
+    assert len(bad) == 0, f"words differ at {len(bad)} queries, first {bad[:5]}"

@@ -1,0 +1,228 @@
+"""GPU parity: the HIP library against the CPU oracle, bit for bit, through the C ABI.
+
+Workloads: the four fit recipes at full size (recipe 4 on a subset of its 64
+identical-shape contexts), random batches covering every feature-word count
+1..64 with rank-deficient and contradictory data, the degenerate contexts the
+method has, and the query streams of the encode recipes.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+import parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def f2(require_gpu):
+    from paper_2608_20532_amd import f2gpu
+    return f2gpu
+
+
+def _fit_and_compare(f2, wl):
+    print(f"fit parity: recipe {wl.recipe}, {wl.num_ctx} contexts, {wl.total_rows} rows", flush=True)
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    parity.compare_fit(model, ref)
+    return model, ref
+
+
+@pytest.mark.parametrize("recipe,num_ctx", [(1, 1), (2, 4096), (3, 80000), (4, 2)])
+def test_fit_recipes(f2, recipe, num_ctx):
+    wl = synth.fit_workload(recipe, num_ctx=num_ctx)
+    model, ref = _fit_and_compare(f2, wl)
+    assert np.array_equal((ref.flags & 1) != 0, wl.contra.astype(bool) & (wl.m_rows >= 2))
+
+
+def _random_batch(seed, widths, max_rows=300):
+    rng = np.random.default_rng(seed)
+    n_bits, rows_list = [], []
+    for n in widths:
+        n = int(n)
+        fw = (n + 64) // 64
+        m = int(rng.choice([0, 1, 2, 63, 64, 65, 127, 129, int(rng.integers(0, max_rows))]))
+        kind = rng.integers(0, 4)
+        d = n + 1
+        # feature vectors from a random pool of k generators (k small -> many dependent rows)
+        k = int(rng.integers(1, min(d, 96) + 1)) if kind else d
+        pool = rng.integers(0, 2 ** 63, size=(k, fw), dtype=np.uint64) ^ (rng.integers(0, 2, size=(k, fw), dtype=np.uint64) << np.uint64(63))
+        Wp = rng.integers(0, 2 ** 63, size=(k, 2), dtype=np.uint64)
+        rows = np.zeros((m, fw + 2), np.uint64)
+        for i in range(m):
+            sel = rng.integers(0, 2, size=k).astype(bool)
+            if kind == 3 and rng.random() < 0.2:
+                sel[:] = False
+            rows[i, :fw] = np.bitwise_xor.reduce(pool[sel], axis=0) if sel.any() else 0
+            rows[i, fw:] = np.bitwise_xor.reduce(Wp[sel], axis=0) if sel.any() else 0
+            if kind == 2 and rng.random() < 0.1:   # flip an output bit: contradictions
+                rows[i, fw + int(rng.integers(0, 2))] ^= np.uint64(1) << np.uint64(int(rng.integers(0, 64)))
+        # junk in padding bits above the constant
+        vb = d - 64 * (fw - 1)
+        if vb < 64 and m:
+            rows[:, fw - 1] |= np.uint64(((1 << 64) - 1) ^ ((1 << vb) - 1)) & rng.integers(0, 2 ** 63, size=m, dtype=np.uint64)
+        n_bits.append(n)
+        rows_list.append(rows)
+    return synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_fit_random_small_widths(f2, seed):
+    rng = np.random.default_rng(seed)
+    widths = list(rng.integers(0, 512, size=300)) + [0, 1, 62, 63, 64, 65, 127, 128, 255, 256, 511]
+    _fit_and_compare(f2, _random_batch(seed, widths))
+
+
+def test_fit_random_large_widths(f2):
+    widths = [512, 575, 576, 1000, 1023, 1024, 2047, 2500, 4094, 4095]
+    _fit_and_compare(f2, _random_batch(77, widths, max_rows=200))
+
+
+def test_fit_degenerate_contexts(f2):
+    """n=0; 0 rows; all-zero rows; zero features with nonzero output; linear (bias 0) rows; duplicates."""
+    rows_list, n_bits = [], []
+    # n = 0: only the constant column
+    n_bits.append(0); rows_list.append(np.array([[1, 5, 0], [1, 5, 0], [1, 6, 0], [0, 0, 0]], np.uint64))
+    # 0 rows
+    n_bits.append(10); rows_list.append(np.zeros((0, 3), np.uint64))
+    # all-zero rows, then zero features with nonzero output
+    n_bits.append(20); rows_list.append(np.array([[0, 0, 0], [0, 0, 0], [0, 1, 0], [0, 0, 1 << 63]], np.uint64))
+    # linear rows (constant 0) and duplicates (App. B shape)
+    n_bits.append(4); rows_list.append(np.array([[12, 159, 0], [8, 165, 0], [10, 102, 0], [6, 249, 0], [6, 248, 0], [12, 159, 0]], np.uint64))
+    # 64-bit boundary: n = 63 (constant at bit 63), n = 64 (constant alone in word 1)
+    n_bits.append(63); rows_list.append(np.array([[(1 << 63) | 5, 1, 2], [(1 << 63) | 3, 4, 8]], np.uint64))
+    n_bits.append(64); rows_list.append(np.array([[5, 1, 1, 2], [3, 1, 4, 8], [0, 1, 7, 7]], np.uint64))
+    wl = synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+    _fit_and_compare(f2, wl)
+
+
+def test_fit_bad_segments_and_widths(f2):
+    """Malformed segments, widths and output offsets are flagged per context; others still fit."""
+    import torch
+    wl = synth.fit_workload(2, num_ctx=8)
+    n_bits = wl.n_bits.copy()
+    row_off = wl.row_off.copy()
+    n_bits[1] = 5000                       # too wide
+    n_bits[2] = -3                         # negative width
+    row_off[4] += 1                        # segment 3 no longer a multiple of the row size (and 4 shifted)
+    layout_n = np.clip(n_bits, 0, oracle.MAX_N)
+    ref = oracle.fit_batch(wl.rows, row_off, n_bits)
+    from paper_2608_20532_amd import f2gpu
+    model = f2gpu.Model(layout_n)
+    model.n_bits = parity.to_dev(n_bits)
+    model._struct = None
+    nb = f2gpu.f2_fit_workspace_bytes(model.num_ctx)
+    ws = f2gpu.workspace(nb)
+    rows_d, off_d = parity.to_dev(wl.rows), parity.to_dev(row_off)
+    assert f2gpu.f2_fit_batch(rows_d, wl.rows.size, off_d, model, ws, nb) == 0
+    torch.cuda.synchronize()
+    g = parity.model_to_host(model)
+    assert g["flags"][1] == oracle.CTX_BAD_WIDTH and g["flags"][2] == oracle.CTX_BAD_WIDTH
+    assert g["flags"][3] == oracle.CTX_BAD_SEGMENT
+    assert np.array_equal(g["flags"], ref.flags) and np.array_equal(g["rank"], ref.rank)
+    # output offsets past the buffers
+    model2 = f2gpu.Model(wl.n_bits)
+    bo = model2.basis_off_host.copy(); bo[5] = int(bo[-1])
+    model2.basis_off = parity.to_dev(bo)
+    model2._struct = None
+    assert f2gpu.f2_fit_batch(parity.to_dev(wl.rows), wl.rows.size, parity.to_dev(wl.row_off), model2, ws, nb) == 0
+    torch.cuda.synchronize()
+    assert parity.host(model2.ctx_flags, np.uint32)[5] == oracle.CTX_BAD_OUTPUT
+
+
+def test_fit_host_errors(f2):
+    from paper_2608_20532_amd import f2gpu
+    wl = synth.fit_workload(1)
+    model = f2gpu.Model(wl.n_bits)
+    nb = f2gpu.f2_fit_workspace_bytes(1)
+    ws = f2gpu.workspace(nb)
+    rows_d, off_d = parity.to_dev(wl.rows), parity.to_dev(wl.row_off)
+    assert f2gpu.f2_fit_batch(rows_d, wl.rows.size, off_d, model, ws, nb - 1) == f2gpu.F2_EWORKSPACE
+    assert f2gpu.f2_fit_batch(rows_d, -1, off_d, model, ws, nb) == f2gpu.F2_EINVAL
+    assert f2gpu.f2_fit_batch(rows_d, wl.rows.size, None, model, ws, nb) == f2gpu.F2_EINVAL
+
+
+def test_fit_deterministic(f2):
+    wl = synth.fit_workload(3, num_ctx=3000)
+    a = parity.model_to_host(parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits))
+    b = parity.model_to_host(parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits))
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    for k in ("rank", "flags", "n_contra", "first"):
+        assert np.array_equal(a[k], b[k])
+    assert np.array_equal(a["maps"], b["maps"])
+
+
+def _encode_and_compare(f2, wl, model, ref, nq, stride, frac, zipf, sample=None):
+    print(f"encode parity: recipe {wl.recipe}, {nq} queries, stride {stride}", flush=True)
+    ctx, x, planted = synth.queries(wl, nq, stride, frac, zipf)
+    words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x), stride)
+    import torch
+    torch.cuda.synchronize()
+    if sample is None:
+        rw, rq = oracle.encode_batch(ref, ctx, x, stride)
+        parity.compare_encode(words, qf, rw, rq)
+    else:
+        xs = x.reshape(nq, stride)[sample].reshape(-1)
+        rw, rq = oracle.encode_batch(ref, ctx[sample], xs, stride)
+        parity.compare_encode(words, qf, rw, rq, sample)
+    return planted
+
+
+@pytest.mark.parametrize("recipe,num_ctx,nq,stride,frac,zipf", [
+    (1, 1, 1000, 1, 0.10, 0.0),
+    (2, 4096, 1_000_000, 2, 0.02, 0.0),
+    (3, 80000, 1_000_000, 4, 0.01, 1.1),
+])
+def test_encode_recipes(f2, recipe, num_ctx, nq, stride, frac, zipf):
+    wl = synth.fit_workload(recipe, num_ctx=num_ctx)
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    _encode_and_compare(f2, wl, model, ref, nq, stride, frac, zipf)
+
+
+def test_encode_random_widths_and_bad_ids(f2):
+    rng = np.random.default_rng(5)
+    widths = list(rng.integers(0, 600, size=60)) + [0, 63, 64, 4095]
+    wl = _random_batch(11, widths, max_rows=120)
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    stride = 64
+    nq = 20000
+    ctx = rng.integers(-2, wl.num_ctx + 2, size=nq).astype(np.int32)
+    x = np.zeros((nq, stride), np.uint64)
+    for i in range(nq):
+        c = int(ctx[i])
+        if not (0 <= c < wl.num_ctx):
+            continue
+        n = int(wl.n_bits[c]); fw = (n + 64) // 64; W = fw + 2
+        m = int(wl.m_rows[c])
+        rows = wl.rows[wl.row_off[c]:wl.row_off[c + 1]].reshape(-1, W)
+        mode = rng.integers(0, 4)
+        if m and mode < 3:   # combination of training rows (constant bit stripped)
+            sel = rows[rng.integers(0, m, size=int(rng.integers(1, 4)))]
+            v = np.bitwise_xor.reduce(sel[:, :fw], axis=0)
+            x[i, :fw] = v
+            x[i, n // 64] &= ~(np.uint64(1) << np.uint64(n % 64))
+        if mode == 2:        # one random bit anywhere in the stride (inside or outside the width)
+            b = int(rng.integers(0, 64 * stride))
+            x[i, b // 64] ^= np.uint64(1) << np.uint64(b % 64)
+        if mode == 3:
+            x[i] = rng.integers(0, 2 ** 63, size=stride, dtype=np.uint64) if rng.random() < 0.5 else 0
+    words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x.reshape(-1)), stride)
+    import torch
+    torch.cuda.synchronize()
+    rw, rq = oracle.encode_batch(ref, ctx, x.reshape(-1), stride)
+    parity.compare_encode(words, qf, rw, rq)
+    assert (rq & oracle.Q_OUT_OF_SPAN).any() and (rq == 0).any() and (rq & oracle.Q_BAD_CTX).any()
+
+
+def test_encode_recipe5_full_size_sampled(f2):
+    """The 100M-query Zipf stream at full size; the oracle checks a random sample of 200k queries."""
+    wl = synth.fit_workload(5)
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    nq, stride, frac, zipf = synth.QUERY_RECIPE[5]
+    sample = np.sort(np.random.default_rng(1).choice(nq, size=200_000, replace=False))
+    planted = _encode_and_compare(f2, wl, model, ref, nq, stride, frac, zipf, sample=sample)
+    assert 0.008 < planted.mean() < 0.012
