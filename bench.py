@@ -54,6 +54,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="recipe2", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build measures one GPU only; run with --gpus 1 "
@@ -65,6 +67,18 @@ def main():
 
     import synth
     from paper_2608_20532_amd import f2gpu
+
+    if args.copy_calibration_mb:
+        # plain copy of a known size: its FETCH_SIZE / WRITE_SIZE readings give the
+        # counter-to-bytes factor used for the roofline traffic figure
+        nbytes = args.copy_calibration_mb << 20
+        src = torch.ones(nbytes // 8, dtype=torch.int64, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 3}), flush=True)
+        return
 
     recipe, num_ctx, nq, stride, frac, zipf = WORKLOADS[args.workload]
     torch.cuda.set_device(0)
@@ -85,7 +99,7 @@ def main():
         ctx_d, x_d = to_dev(ctx), to_dev(x)
         words = torch.empty((nq, 2), dtype=torch.int64, device=dev)
         qf = torch.empty(nq, dtype=torch.uint8, device=dev)
-        ews = f2gpu.f2_encode_workspace_bytes(model)
+        ews = f2gpu.f2_encode_workspace_bytes(model, nq)
         enc_ws = f2gpu.workspace(ews, dev)
     stream = torch.cuda.current_stream()
     sptr = stream.cuda_stream

@@ -134,8 +134,14 @@ size_t f2_fit_workspace_bytes(int32_t num_ctx);
 int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* model_host,
                  void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes f2_encode_batch needs for a fitted model (encode tables mirror the basis capacity). */
-size_t f2_encode_workspace_bytes(const f2_model* model_host);
+/*
+ * Workspace bytes f2_encode_batch needs for a fitted model and a batch size:
+ * the per-context parity-check rows on the free columns (within the basis
+ * capacity) and a zero column.  The batch size is part of the signature so the
+ * encode path may use per-query scratch without an ABI change; the current one
+ * needs none.
+ */
+size_t f2_encode_workspace_bytes(const f2_model* model_host, int64_t num_queries);
 
 /*
  * Encode a batch of queries against a fitted model (Sec. 2.3).

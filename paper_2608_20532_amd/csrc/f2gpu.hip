@@ -32,12 +32,10 @@
 
 namespace {
 
-constexpr int kClasses = 5;          // feature words 1, 2, 3-4, 5-8, >8
 constexpr int kLargeRows = 64;       // rows per block, large path
 constexpr int kLargeThreads = 256;
 constexpr int kMaxW = 66;            // widest row: 64 feature words + 2 output words
 constexpr int kEncThreads = 256;
-constexpr int kEncHW = 8;            // parity-check words kept in registers
 
 struct FitArgs {
     const uint64_t* rows;
@@ -56,8 +54,6 @@ struct FitArgs {
     uint32_t* ctx_flags;
     int32_t* n_contra;
     int64_t* first_contra;
-    int32_t* counters;  // [0, kClasses): contexts per class
-    int32_t* lists;     // kClasses x num_ctx context ids
 };
 
 struct EncArgs {
@@ -69,7 +65,10 @@ struct EncArgs {
     const int32_t* pivots;
     const int32_t* rank;
     const uint32_t* ctx_flags;
-    uint64_t* tables;  // same offsets as the basis: context c at basis_off[c]
+    const int64_t* map_off;
+    const uint64_t* maps;
+    uint64_t* tables;   // parity-check rows, context c at basis_off[c]
+    int64_t zero_word;  // tables[zero_word .. +2) is a zero column
     const int32_t* ctx_id;
     const uint64_t* x;
     int32_t stride;
@@ -104,223 +103,493 @@ __device__ __forceinline__ uint64_t top_mask(int n, int fw) {
 }
 
 // ---------------------------------------------------------------------------
-// plan: validate every context, write the outputs of invalid ones, and sort
-// the valid ones into width classes.
+// context validation, shared by the fit kernels: a context is fitted by the
+// kernel of its width class; an invalid one gets rank 0 and a flag, written by
+// the register-basis kernel.  Each workgroup owns contexts g, g + G, g + 2G, ...
+// (G = grid size) and reads their descriptors 64 at a time, one per lane.
 // ---------------------------------------------------------------------------
-__global__ void k_fit_init(int32_t* counters) {
-    if (threadIdx.x < 16) counters[threadIdx.x] = 0;
+struct CtxDesc {
+    int c, n;
+    uint32_t bad;
+    int64_t row0, m;
+};
+
+__device__ __forceinline__ CtxDesc load_desc(const FitArgs& a, int64_t c) {
+    CtxDesc ds{-1, -1, 0u, 0, 0};  // c = -1: no context
+    if (c >= a.num_ctx) return ds;
+    ds.c = static_cast<int>(c);
+    const int n = a.n_bits[c];
+    ds.n = n;
+    if (n < 0 || n > F2_MAX_N_BITS) {
+        ds.bad = F2_CTX_BAD_WIDTH;
+        return ds;
+    }
+    const int d = n + 1;
+    const int W = feat_words(n) + F2_Y_WORDS;
+    const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
+    if (bo < 0 || bo + static_cast<int64_t>(d) * W > a.basis_words || po < 0 || po + d > a.piv_entries || mo < 0 ||
+        mo + 2 * static_cast<int64_t>(d) > a.map_words) {
+        ds.bad = F2_CTX_BAD_OUTPUT;
+        return ds;
+    }
+    const int64_t s0 = a.row_off[c], s1 = a.row_off[c + 1];
+    if (s0 < 0 || s1 < s0 || s1 > a.rows_words || (s1 - s0) % W != 0) {
+        ds.bad = F2_CTX_BAD_SEGMENT;
+        return ds;
+    }
+    ds.row0 = s0;
+    ds.m = (s1 - s0) / W;
+    return ds;
 }
 
-__global__ __launch_bounds__(256) void k_fit_plan(FitArgs a) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    int cls = -1;
-    if (c < a.num_ctx) {
-        const int n = a.n_bits[c];
-        uint32_t flags = 0;
-        int64_t mo = 0;
-        int d = 0;
-        if (n < 0 || n > F2_MAX_N_BITS) {
-            flags = F2_CTX_BAD_WIDTH;
-        } else {
-            d = n + 1;
-            const int W = feat_words(n) + F2_Y_WORDS;
-            const int64_t bo = a.basis_off[c], po = a.piv_off[c];
-            mo = a.map_off[c];
-            if (bo < 0 || bo + static_cast<int64_t>(d) * W > a.basis_words || po < 0 || po + d > a.piv_entries ||
-                mo < 0 || mo + 2 * static_cast<int64_t>(d) > a.map_words) {
-                flags = F2_CTX_BAD_OUTPUT;
-            } else {
-                const int64_t s0 = a.row_off[c], s1 = a.row_off[c + 1];
-                if (s0 < 0 || s1 < s0 || s1 > a.rows_words || (s1 - s0) % W != 0) flags = F2_CTX_BAD_SEGMENT;
-            }
-        }
-        if (flags) {
-            a.rank[c] = 0;
-            a.n_contra[c] = 0;
-            a.first_contra[c] = -1;
-            a.ctx_flags[c] = flags;
-            if (flags == F2_CTX_BAD_SEGMENT)
-                for (int j = 0; j < 2 * d; ++j) a.maps[mo + j] = 0;
-        } else {
-            const int fw = feat_words(n);
-            cls = fw == 1 ? 0 : fw == 2 ? 1 : fw <= 4 ? 2 : fw <= 8 ? 3 : 4;
-        }
-    }
-    // wave-aggregated append: one atomic per class per wavefront
+__device__ __forceinline__ CtxDesc readlane_desc(const CtxDesc& v, int t) {
+    CtxDesc ds;
+    ds.c = __builtin_amdgcn_readlane(v.c, t);
+    ds.n = __builtin_amdgcn_readlane(v.n, t);
+    ds.bad = __builtin_amdgcn_readlane(v.bad, t);
+    ds.row0 = static_cast<int64_t>(readlane64(static_cast<uint64_t>(v.row0), t));
+    ds.m = static_cast<int64_t>(readlane64(static_cast<uint64_t>(v.m), t));
+    return ds;
+}
+
+// width class of a valid context: 0 register basis (fw 1-3), 1 LDS basis (fw 4-8), 2 large
+__device__ __forceinline__ int width_class(int n) {
+    const int fw = feat_words(n);
+    return fw <= 3 ? 0 : fw <= 8 ? 1 : 2;
+}
+
+// outputs of an invalid context (all lanes of one wavefront)
+__device__ void write_bad_context(const FitArgs& a, const CtxDesc& ds) {
     const int lane = threadIdx.x & 63;
-    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    for (int k = 0; k < kClasses; ++k) {
-        const uint64_t mask = __ballot(cls == k);
-        if (!mask) continue;
-        int base = 0;
-        const int leader = ffs64(mask);
-        if (lane == leader) base = atomicAdd(&a.counters[k], __popcll(mask));
-        base = __shfl(base, leader);
-        if (cls == k) a.lists[static_cast<int64_t>(k) * a.num_ctx + base + __popcll(mask & below)] = c;
+    if (lane == 0) {
+        a.rank[ds.c] = 0;
+        a.n_contra[ds.c] = 0;
+        a.first_contra[ds.c] = -1;
+        a.ctx_flags[ds.c] = ds.bad;
+    }
+    if (ds.bad == F2_CTX_BAD_SEGMENT) {
+        const int64_t mo = a.map_off[ds.c];
+        for (int j = lane; j < 2 * (ds.n + 1); j += 64) a.maps[mo + j] = 0;
     }
 }
 
 // ---------------------------------------------------------------------------
-// small-context fit: one wavefront per context, basis in LDS, FW = feature
-// words of the class (contexts of the class have fw <= FW)
+// register-basis fit (fw <= 3): one wavefront per context.  Lane s of register
+// set k holds retained row 64k + s (fw + 2 words and its pivot); the rows of
+// the current block are one per lane.  An LDS mirror of the retained rows
+// feeds the block reduce with broadcast reads.
 // ---------------------------------------------------------------------------
 template <int FW>
-__device__ __forceinline__ uint64_t pick_word(const uint64_t (&f)[FW], int w) {
-    uint64_t v = f[0];
-#pragma unroll
-    for (int k = 1; k < FW; ++k) v = (w == k) ? f[k] : v;
-    return v;
+__device__ __forceinline__ uint64_t word_at(const uint64_t (&f)[FW], int wi) {
+    // branch-free select of word wi (wi is usually wavefront-uniform)
+    if constexpr (FW == 1) {
+        return f[0];
+    } else if constexpr (FW == 2) {
+        const uint64_t s1 = 0ull - static_cast<uint64_t>(wi == 1);
+        return f[0] ^ ((f[0] ^ f[1]) & s1);
+    } else {
+        static_assert(FW == 3, "register basis holds at most 3 feature words");
+        const uint64_t s1 = 0ull - static_cast<uint64_t>(wi == 1);
+        const uint64_t s2 = 0ull - static_cast<uint64_t>(wi == 2);
+        return f[0] ^ ((f[0] ^ f[1]) & s1) ^ ((f[0] ^ f[2]) & s2);
+    }
 }
 
+// all-ones when bit b of w is set, else zero (32-bit: one mask serves both halves)
+__device__ __forceinline__ uint32_t bit_mask(uint64_t w, int b) {
+    const uint32_t dw = (b & 32) ? static_cast<uint32_t>(w >> 32) : static_cast<uint32_t>(w);
+    return static_cast<uint32_t>(static_cast<int32_t>(dw << (31 - (b & 31))) >> 31);
+}
+
+// f ^ (m & d) with m a 32-bit all-ones/zero mask: one v_bitop3 per half
+__device__ __forceinline__ uint64_t xor_and(uint64_t f, uint32_t m, uint64_t d) {
+    const uint32_t lo = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(f), m, static_cast<uint32_t>(d), 0x78);
+    const uint32_t hi =
+        __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(f >> 32), m, static_cast<uint32_t>(d >> 32), 0x78);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+constexpr int kRegMaxFW = 3;
+constexpr int kRecWords = 6;  // LDS record: fw feature words, 2 output words, pivot (<= 6 words)
+
 template <int FW>
-__global__ __launch_bounds__(64) void k_fit_small(FitArgs a, int cls) {
-    constexpr int CAP = 64 * FW;  // d <= 64 FW retained rows at most
-    __shared__ uint64_t sBf[FW][CAP];
-    __shared__ uint64_t sBy[2][CAP];
-    __shared__ int16_t sPiv[CAP];
-    __shared__ int16_t sPos[CAP];
+__device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec, int16_t* sPos) {
+    constexpr int W = FW + F2_Y_WORDS;
+    constexpr int NS = FW;  // register sets: d <= 64 FW retained rows
     const int lane = threadIdx.x;
-    const int count = a.counters[cls];
-    const int32_t* list = a.lists + static_cast<int64_t>(cls) * a.num_ctx;
+    const int c = ds.c, n = ds.n, d = n + 1;
+    const int64_t m = ds.m;
+    const uint64_t* R = a.rows + ds.row0;
+    const uint64_t tmask = top_mask(n, FW);
+    const int cw = n >> 6;
+    const uint64_t cbit = 1ull << (n & 63);
 
-    for (int idx = blockIdx.x; idx < count; idx += gridDim.x) {
-        const int c = list[idx];
-        const int n = a.n_bits[c];
-        const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
-        const int64_t s0 = a.row_off[c];
-        const int64_t m = (a.row_off[c + 1] - s0) / W;
-        const uint64_t* R = a.rows + s0;
-        const uint64_t tmask = top_mask(n, fw);
-        const int cw = n >> 6;
-        const uint64_t cbit = 1ull << (n & 63);
+    for (int j = lane; j < d; j += 64) sPos[j] = -1;
+    uint64_t bf[NS][FW], by0[NS], by1[NS];
+    int bp[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+#pragma unroll
+        for (int w = 0; w < FW; ++w) bf[k][w] = 0;
+        by0[k] = by1[k] = 0;
+        bp[k] = 0;
+    }
+    uint64_t pm[FW];  // pivot columns (uniform)
+#pragma unroll
+    for (int w = 0; w < FW; ++w) pm[w] = 0;
+    int rank = 0, ncontra = 0;
+    int64_t first = -1;
 
-        for (int j = lane; j < d; j += 64) sPos[j] = -1;
-        int rank = 0, ncontra = 0;
-        int64_t first = -1;
-        __syncthreads();
-
-        for (int64_t b0 = 0; b0 < m; b0 += 64) {
-            const int64_t i = b0 + lane;
-            const bool valid = i < m;
-            uint64_t f[FW];
-            uint64_t y0 = 0, y1 = 0;
+    auto store_mirror = [&]() {
 #pragma unroll
-            for (int w = 0; w < FW; ++w) f[w] = 0;
-            if (valid) {
-                const uint64_t* row = R + i * W;
+        for (int k = 0; k < NS; ++k) {
+            const int s = 64 * k + lane;
+            if (s < rank) {
+                uint64_t* rec = sRec + s * kRecWords;
 #pragma unroll
-                for (int w = 0; w < FW; ++w)
-                    if (w < fw) f[w] = row[w];
-                y0 = row[fw];
-                y1 = row[fw + 1];
-#pragma unroll
-                for (int w = 0; w < FW; ++w)
-                    if (w == fw - 1) f[w] &= tmask;
+                for (int w = 0; w < FW; ++w) rec[w] = bf[k][w];
+                rec[FW] = by0[k];
+                rec[FW + 1] = by1[k];
+                rec[W] = static_cast<uint64_t>(bp[k]);
             }
-            // (1) reduce against the retained basis (one pass: it is fully reduced)
-            for (int s = 0; s < rank; ++s) {
-                const int p = sPiv[s];
-                if ((pick_word<FW>(f, p >> 6) >> (p & 63)) & 1ull) {
+        }
+    };
+
+    for (int64_t b0 = 0; b0 < m; b0 += 64) {
+        const int64_t i = b0 + lane;
+        const bool valid = i < m;
+        uint64_t f[FW], y0 = 0, y1 = 0;
 #pragma unroll
-                    for (int w = 0; w < FW; ++w) f[w] ^= sBf[w][s];
-                    y0 ^= sBy[0][s];
-                    y1 ^= sBy[1][s];
-                }
+        for (int w = 0; w < FW; ++w) f[w] = 0;
+        if (valid) {
+            const uint64_t* row = R + i * W;
+#pragma unroll
+            for (int w = 0; w < FW; ++w) f[w] = row[w];
+            y0 = row[FW];
+            y1 = row[FW + 1];
+            f[FW - 1] &= tmask;
+        }
+
+        // (1) reduce against the retained basis: it is fully reduced, so the
+        //     row's own (unreduced) bits at the pivot columns select the rows to
+        //     add; the selection masks do not depend on one another
+        uint64_t f0[FW];
+#pragma unroll
+        for (int w = 0; w < FW; ++w) f0[w] = f[w];
+        int s = 0;
+        for (; s + 4 <= rank; s += 4) {
+            uint64_t rv[4][W];
+            int pv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint64_t* rec = sRec + (s + u) * kRecWords;
+#pragma unroll
+                for (int w = 0; w < W; ++w) rv[u][w] = rec[w];
+                pv[u] = static_cast<int>(rec[W]);
             }
-            // (2) in-block elimination in stream order
-            uint64_t pending = __ballot(valid);
-            while (pending) {
-                bool nzf = false;
 #pragma unroll
-                for (int w = 0; w < FW; ++w) nzf |= (f[w] != 0);
-                const uint64_t nz = __ballot(nzf) & pending;
-                const int j = nz ? ffs64(nz) : 64;
-                const uint64_t before = (j >= 64) ? pending : (pending & ((1ull << j) - 1));
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t mm = bit_mask(word_at<FW>(f0, pv[u] >> 6), pv[u] & 63);
+#pragma unroll
+                for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, rv[u][w]);
+                y0 = xor_and(y0, mm, rv[u][FW]);
+                y1 = xor_and(y1, mm, rv[u][FW + 1]);
+            }
+        }
+        for (; s < rank; ++s) {
+            const uint64_t* rec = sRec + s * kRecWords;
+            const int p = static_cast<int>(rec[W]);
+            const uint32_t mm = bit_mask(word_at<FW>(f0, p >> 6), p & 63);
+#pragma unroll
+            for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, rec[w]);
+            y0 = xor_and(y0, mm, rec[FW]);
+            y1 = xor_and(y1, mm, rec[FW + 1]);
+        }
+
+        // (2) in-block elimination in stream order
+        uint64_t pending = __ballot(valid);
+        bool changed = false;
+        while (pending) {
+            uint64_t any = f[0];
+#pragma unroll
+            for (int w = 1; w < FW; ++w) any |= f[w];
+            const uint64_t nz = __ballot(any != 0) & pending;
+            const int j = nz ? ffs64(nz) : 64;
+            const uint64_t before = (j >= 64) ? pending : (pending & ((1ull << j) - 1));
+            if (before) {
+                // zero-feature residuals: redundant, or contradictory when the output is nonzero
                 const uint64_t cm = __ballot((y0 | y1) != 0) & before;
                 if (cm) {
                     if (ncontra == 0) first = b0 + ffs64(cm);
                     ncontra += __popcll(cm);
                 }
                 pending &= ~before;
-                if (j >= 64) break;
-                uint64_t F[FW];
+            }
+            if (j >= 64) break;
+            uint64_t F[FW];
 #pragma unroll
-                for (int w = 0; w < FW; ++w) F[w] = readlane64(f[w], j);
-                const uint64_t Y0 = readlane64(y0, j), Y1 = readlane64(y1, j);
-                // pivot: highest-priority set feature bit (x_{n-1} .. x_0, then the constant)
-                int p = -1;
+            for (int w = 0; w < FW; ++w) F[w] = readlane64(f[w], j);
+            const uint64_t Y0 = readlane64(y0, j), Y1 = readlane64(y1, j);
+            // pivot: highest-priority set feature bit (x_{n-1} .. x_0, then the constant)
+            int p = -1;
 #pragma unroll
-                for (int w = FW - 1; w >= 0; --w) {
-                    uint64_t v = F[w];
-                    if (w == cw) v &= ~cbit;
-                    if (p < 0 && v) p = 64 * w + msb64(v);
+            for (int w = FW - 1; w >= 0; --w) {
+                const uint64_t v = (w == cw) ? (F[w] & ~cbit) : F[w];
+                if (p < 0 && v) p = 64 * w + msb64(v);
+            }
+            if (p < 0) p = n;
+            const int pw = p >> 6, pb = p & 63;
+            {  // rows of the block that hold bit p (rows no longer pending are never read again)
+                const uint32_t mm = bit_mask(word_at<FW>(f, pw), pb);
+#pragma unroll
+                for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, F[w]);
+                y0 = xor_and(y0, mm, Y0);
+                y1 = xor_and(y1, mm, Y1);
+            }
+#pragma unroll
+            for (int k = 0; k < NS; ++k) {  // clear p from the retained rows
+                if (64 * k < rank) {
+                    const uint32_t mm = bit_mask(word_at<FW>(bf[k], pw), pb);
+#pragma unroll
+                    for (int w = 0; w < FW; ++w) bf[k][w] = xor_and(bf[k][w], mm, F[w]);
+                    by0[k] = xor_and(by0[k], mm, Y0);
+                    by1[k] = xor_and(by1[k], mm, Y1);
                 }
-                if (p < 0) p = n;
-                // later rows of the block holding bit p
-                if (lane > j && ((pick_word<FW>(f, p >> 6) >> (p & 63)) & 1ull)) {
+            }
+            {  // insert at slot `rank`
+                const int ks = rank >> 6;
+                const bool me = lane == (rank & 63);
 #pragma unroll
-                    for (int w = 0; w < FW; ++w) f[w] ^= F[w];
-                    y0 ^= Y0;
-                    y1 ^= Y1;
-                }
-                // clear p from every retained row, then insert
-                for (int s = lane; s < rank; s += 64) {
-                    if ((sBf[p >> 6][s] >> (p & 63)) & 1ull) {
+                for (int k = 0; k < NS; ++k) {
+                    if (k == ks && me) {
 #pragma unroll
-                        for (int w = 0; w < FW; ++w) sBf[w][s] ^= F[w];
-                        sBy[0][s] ^= Y0;
-                        sBy[1][s] ^= Y1;
+                        for (int w = 0; w < FW; ++w) bf[k][w] = F[w];
+                        by0[k] = Y0;
+                        by1[k] = Y1;
+                        bp[k] = p;
                     }
                 }
-                if (lane == 0) {
+            }
 #pragma unroll
-                    for (int w = 0; w < FW; ++w) sBf[w][rank] = F[w];
-                    sBy[0][rank] = Y0;
-                    sBy[1][rank] = Y1;
-                    sPiv[rank] = static_cast<int16_t>(p);
-                    sPos[p] = static_cast<int16_t>(rank);
-                }
-                ++rank;
-                pending &= ~(1ull << j);
-                __syncthreads();
-            }
+            for (int w = 0; w < FW; ++w)
+                if (w == pw) pm[w] |= 1ull << pb;
+            if (lane == 0) sPos[p] = static_cast<int16_t>(rank);
+            ++rank;
+            pending &= ~(1ull << j);
+            changed = true;
         }
-        __syncthreads();
+        if (changed && b0 + 64 < m) {
+            store_mirror();
+            __syncthreads();
+        }
+    }
 
-        // outputs: basis rows and pivots in descending priority, canonical map, scalars
-        const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
-        for (int s = lane; s < rank; s += 64) {
-            const int p = sPiv[s];
-            int k = 0;
-            if (p == n) {
-                k = rank - 1;
-            } else {
-                for (int t = 0; t < rank; ++t) {
-                    const int q = sPiv[t];
-                    k += (q > p && q < n);
+    // outputs: basis rows and pivots in descending priority, canonical map, scalars
+    store_mirror();
+    __syncthreads();
+    const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+        const int s = 64 * k + lane;
+        if (s < rank) {
+            const int p = bp[k];
+            int kout = rank - 1;
+            if (p != n) {  // pivots of higher priority: x bits above p
+                kout = 0;
+#pragma unroll
+                for (int w = 0; w < FW; ++w) {
+                    uint64_t v = pm[w];
+                    if (w == cw) v &= ~cbit;
+                    if (w < (p >> 6)) v = 0;
+                    if (w == (p >> 6)) v &= ((p & 63) == 63) ? 0ull : (~0ull << ((p & 63) + 1));
+                    kout += __popcll(v);
                 }
             }
-            uint64_t* out = a.basis + bo + static_cast<int64_t>(k) * W;
-            for (int w = 0; w < fw; ++w) out[w] = sBf[w][s];
-            out[fw] = sBy[0][s];
-            out[fw + 1] = sBy[1][s];
-            a.pivots[po + k] = p;
+            uint64_t* out = a.basis + bo + static_cast<int64_t>(kout) * W;
+#pragma unroll
+            for (int w = 0; w < FW; ++w) out[w] = bf[k][w];
+            out[FW] = by0[k];
+            out[FW + 1] = by1[k];
+            a.pivots[po + kout] = p;
         }
-        for (int j = lane; j < d; j += 64) {
-            const int s = sPos[j];
-            a.maps[mo + 2 * j] = s >= 0 ? sBy[0][s] : 0ull;
-            a.maps[mo + 2 * j + 1] = s >= 0 ? sBy[1][s] : 0ull;
+    }
+    for (int j = lane; j < d; j += 64) {
+        const int sl = sPos[j];
+        a.maps[mo + 2 * j] = sl >= 0 ? sRec[sl * kRecWords + FW] : 0ull;
+        a.maps[mo + 2 * j + 1] = sl >= 0 ? sRec[sl * kRecWords + FW + 1] : 0ull;
+    }
+    if (lane == 0) {
+        a.rank[c] = rank;
+        a.n_contra[c] = ncontra;
+        a.first_contra[c] = first;
+        a.ctx_flags[c] = ncontra ? F2_CTX_CONTRADICTION : 0u;
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(64) void k_fit_reg(FitArgs a) {
+    __shared__ __align__(16) uint64_t sRec[64 * kRegMaxFW * kRecWords];
+    __shared__ int16_t sPos[64 * kRegMaxFW];
+    const int lane = threadIdx.x;
+    for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
+        const CtxDesc mine = load_desc(a, blockIdx.x + (k0 + lane) * gridDim.x);
+        uint64_t todo = __ballot(mine.c >= 0 && (mine.bad || width_class(mine.n) == 0));
+        while (todo) {
+            const int t = ffs64(todo);
+            todo &= todo - 1;
+            const CtxDesc ds = readlane_desc(mine, t);
+            if (ds.bad) {
+                write_bad_context(a, ds);
+                continue;
+            }
+            switch (feat_words(ds.n)) {
+                case 1: fit_ctx_reg<1>(a, ds, sRec, sPos); break;
+                case 2: fit_ctx_reg<2>(a, ds, sRec, sPos); break;
+                default: fit_ctx_reg<3>(a, ds, sRec, sPos); break;
+            }
         }
-        if (lane == 0) {
-            a.rank[c] = rank;
-            a.n_contra[c] = ncontra;
-            a.first_contra[c] = first;
-            a.ctx_flags[c] = ncontra ? F2_CTX_CONTRADICTION : 0u;
-        }
-        __syncthreads();
     }
 }
 
+// ---------------------------------------------------------------------------
+// LDS-basis fit (fw 4-8): one wavefront per context, retained rows in LDS
+// ---------------------------------------------------------------------------
+constexpr int kLdsFW = 8;
+
+__global__ __launch_bounds__(64) void k_fit_lds(FitArgs a) {
+    constexpr int FW = kLdsFW;
+    constexpr int CAP = 64 * FW;
+    __shared__ uint64_t sBf[FW][CAP];
+    __shared__ uint64_t sBy[2][CAP];
+    __shared__ int16_t sPiv[CAP];
+    __shared__ int16_t sPos[CAP];
+    __shared__ uint64_t sRow[64][FW];  // this lane's block row (kept in LDS: dynamic word index)
+    const int lane = threadIdx.x;
+
+    for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
+        const CtxDesc mine = load_desc(a, blockIdx.x + (k0 + lane) * gridDim.x);
+        uint64_t todo = __ballot(mine.c >= 0 && !mine.bad && width_class(mine.n) == 1);
+        while (todo) {
+            const int t = ffs64(todo);
+            todo &= todo - 1;
+            const CtxDesc ds = readlane_desc(mine, t);
+            const int c = ds.c, n = ds.n;
+            const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
+            const int64_t m = ds.m;
+            const uint64_t* R = a.rows + ds.row0;
+            const uint64_t tmask = top_mask(n, fw);
+            const int cw = n >> 6;
+            const uint64_t cbit = 1ull << (n & 63);
+            uint64_t* f = sRow[lane];
+
+            for (int j = lane; j < d; j += 64) sPos[j] = -1;
+            int rank = 0, ncontra = 0;
+            int64_t first = -1;
+            __syncthreads();
+
+            for (int64_t b0 = 0; b0 < m; b0 += 64) {
+                const int64_t i = b0 + lane;
+                const bool valid = i < m;
+                uint64_t y0 = 0, y1 = 0;
+                for (int w = 0; w < FW; ++w) f[w] = 0;
+                if (valid) {
+                    const uint64_t* row = R + i * W;
+                    for (int w = 0; w < fw; ++w) f[w] = row[w];
+                    y0 = row[fw];
+                    y1 = row[fw + 1];
+                    f[fw - 1] &= tmask;
+                }
+                for (int s = 0; s < rank; ++s) {
+                    const int p = sPiv[s];
+                    if ((f[p >> 6] >> (p & 63)) & 1ull) {
+                        for (int w = 0; w < fw; ++w) f[w] ^= sBf[w][s];
+                        y0 ^= sBy[0][s];
+                        y1 ^= sBy[1][s];
+                    }
+                }
+                uint64_t pending = __ballot(valid);
+                while (pending) {
+                    uint64_t any = 0;
+                    for (int w = 0; w < fw; ++w) any |= f[w];
+                    const uint64_t nz = __ballot(any != 0) & pending;
+                    const int j = nz ? ffs64(nz) : 64;
+                    const uint64_t before = (j >= 64) ? pending : (pending & ((1ull << j) - 1));
+                    const uint64_t cm = __ballot((y0 | y1) != 0) & before;
+                    if (cm) {
+                        if (ncontra == 0) first = b0 + ffs64(cm);
+                        ncontra += __popcll(cm);
+                    }
+                    pending &= ~before;
+                    if (j >= 64) break;
+                    __syncthreads();
+                    const uint64_t* Fj = sRow[j];
+                    const uint64_t Y0 = readlane64(y0, j), Y1 = readlane64(y1, j);
+                    int p = -1;
+                    for (int w = fw - 1; w >= 0 && p < 0; --w) {
+                        const uint64_t v = (w == cw) ? (Fj[w] & ~cbit) : Fj[w];
+                        if (v) p = 64 * w + msb64(v);
+                    }
+                    if (p < 0) p = n;
+                    if (lane > j && ((f[p >> 6] >> (p & 63)) & 1ull)) {
+                        for (int w = 0; w < fw; ++w) f[w] ^= Fj[w];
+                        y0 ^= Y0;
+                        y1 ^= Y1;
+                    }
+                    for (int s = lane; s < rank; s += 64) {
+                        if ((sBf[p >> 6][s] >> (p & 63)) & 1ull) {
+                            for (int w = 0; w < fw; ++w) sBf[w][s] ^= Fj[w];
+                            sBy[0][s] ^= Y0;
+                            sBy[1][s] ^= Y1;
+                        }
+                    }
+                    if (lane == 0) {
+                        for (int w = 0; w < fw; ++w) sBf[w][rank] = Fj[w];
+                        for (int w = fw; w < FW; ++w) sBf[w][rank] = 0;
+                        sBy[0][rank] = Y0;
+                        sBy[1][rank] = Y1;
+                        sPiv[rank] = static_cast<int16_t>(p);
+                        sPos[p] = static_cast<int16_t>(rank);
+                    }
+                    ++rank;
+                    pending &= ~(1ull << j);
+                    __syncthreads();
+                }
+                __syncthreads();
+            }
+
+            const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
+            for (int s = lane; s < rank; s += 64) {
+                const int p = sPiv[s];
+                int k = 0;
+                if (p == n) {
+                    k = rank - 1;
+                } else {
+                    for (int t2 = 0; t2 < rank; ++t2) {
+                        const int q = sPiv[t2];
+                        k += (q > p && q < n);
+                    }
+                }
+                uint64_t* out = a.basis + bo + static_cast<int64_t>(k) * W;
+                for (int w = 0; w < fw; ++w) out[w] = sBf[w][s];
+                out[fw] = sBy[0][s];
+                out[fw + 1] = sBy[1][s];
+                a.pivots[po + k] = p;
+            }
+            for (int j = lane; j < d; j += 64) {
+                const int s = sPos[j];
+                a.maps[mo + 2 * j] = s >= 0 ? sBy[0][s] : 0ull;
+                a.maps[mo + 2 * j + 1] = s >= 0 ? sBy[1][s] : 0ull;
+            }
+            if (lane == 0) {
+                a.rank[c] = rank;
+                a.n_contra[c] = ncontra;
+                a.first_contra[c] = first;
+                a.ctx_flags[c] = ncontra ? F2_CTX_CONTRADICTION : 0u;
+            }
+            __syncthreads();
+        }
+    }
+}
 // ---------------------------------------------------------------------------
 // large-context fit: one workgroup of 4 wavefronts per context.  The working
 // basis lives in the caller's basis buffer, one slot per priority position
@@ -330,7 +599,7 @@ __global__ __launch_bounds__(64) void k_fit_small(FitArgs a, int cls) {
 __device__ __forceinline__ int prio_slot(int p, int n) { return p < n ? n - 1 - p : n; }
 __device__ __forceinline__ int slot_pivot(int t, int n) { return t < n ? n - 1 - t : n; }
 
-__global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a, int cls) {
+__global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
     __shared__ uint64_t sRow[kLargeRows][kMaxW];
     __shared__ uint64_t sPmask[64];
     __shared__ int sNewRow[kLargeRows];  // block row of the k-th new pivot
@@ -338,16 +607,20 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a, int cls)
     __shared__ int sP, sNumNew, sContra;
     __shared__ long long sFirst;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int count = a.counters[cls];
-    const int32_t* list = a.lists + static_cast<int64_t>(cls) * a.num_ctx;
 
-    for (int idx = blockIdx.x; idx < count; idx += gridDim.x) {
-        const int c = list[idx];
-        const int n = a.n_bits[c];
+    for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
+      // every wavefront reads the same 64 descriptors, so the ballot is uniform across the workgroup
+      const CtxDesc mine = load_desc(a, blockIdx.x + (k0 + lane) * gridDim.x);
+      uint64_t todo = __ballot(mine.c >= 0 && !mine.bad && width_class(mine.n) == 2);
+      while (todo) {
+        const int tt = ffs64(todo);
+        todo &= todo - 1;
+        const CtxDesc ds = readlane_desc(mine, tt);
+        const int c = ds.c;
+        const int n = ds.n;
         const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
-        const int64_t s0 = a.row_off[c];
-        const int64_t m = (a.row_off[c + 1] - s0) / W;
-        const uint64_t* R = a.rows + s0;
+        const int64_t m = ds.m;
+        const uint64_t* R = a.rows + ds.row0;
         const uint64_t tmask = top_mask(n, fw);
         const int cw = n >> 6;
         const uint64_t cbit = 1ull << (n & 63);
@@ -528,34 +801,40 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a, int cls)
             a.ctx_flags[c] = sContra ? F2_CTX_CONTRADICTION : 0u;
         }
         __syncthreads();
+      }
     }
 }
 
 // ---------------------------------------------------------------------------
-// encode tables: entry j of context c (stride 2 + hw words, hw = ceil((d-rank)/64)):
-//   pivot column j  : [z_j | the bits of r_j at the free columns, compacted]
-//   free column j   : [0   | the unit vector of j among the free columns]
+// encode.  T(phi) is the XOR of the canonical map columns M[j] over the set
+// feature bits j of phi = [x | 1] (M[p] = z_p on pivots, 0 elsewhere).  The
+// support test uses the parity check on the free (non-pivot) columns: for each
+// free column f, h_f = e_f + sum over pivots p of r_p[f] e_p; phi lies in the
+// span exactly when every h_f has even overlap with phi (the reduction residual
+// at f is that overlap).  k_enc_prepare writes the rows h_f of each context
+// (fw words each, in ascending f) into the workspace at the basis offsets.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_enc_prepare(EncArgs e) {
     __shared__ uint64_t sFree[64];
     __shared__ int sFreeBefore[65];
-    __shared__ int16_t sSlot[F2_MAX_N_BITS + 1];
+    __shared__ uint64_t sH[64][64];  // one parity-check row per lane
     const int c = blockIdx.x, lane = threadIdx.x;
+    if (c >= e.num_ctx) return;
+    if (c == 0 && lane < 2) e.tables[e.zero_word + lane] = 0;  // a zero 16-byte column
     if (e.ctx_flags[c] & kBadCtx) return;
     const int n = e.n_bits[c];
     const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
     const int r = min(max(e.rank[c], 0), d);  // a model from f2_fit_batch always satisfies 0 <= rank <= d
-    const int hw = (d - r + 63) >> 6, ES = 2 + hw;
+    const int t = d - r;
+    if (t == 0) return;
     const uint64_t* B = e.basis + e.basis_off[c];
     const int32_t* piv = e.pivots + e.piv_off[c];
-    uint64_t* T = e.tables + e.basis_off[c];
+    uint64_t* H = e.tables + e.basis_off[c];
     const uint64_t tmask = top_mask(n, fw);
     for (int w = lane; w < fw; w += 64) sFree[w] = (w == fw - 1) ? tmask : ~0ull;
-    for (int j = lane; j < d; j += 64) sSlot[j] = -1;
     __syncthreads();
     for (int k = lane; k < r; k += 64) {
         const int p = min(max(piv[k], 0), n);
-        sSlot[p] = static_cast<int16_t>(k);
         atomicAnd(reinterpret_cast<unsigned long long*>(&sFree[p >> 6]), ~(1ull << (p & 63)));
     }
     __syncthreads();
@@ -565,36 +844,154 @@ __global__ __launch_bounds__(64) void k_enc_prepare(EncArgs e) {
             sFreeBefore[w] = acc;
             acc += __popcll(sFree[w]);
         }
+        sFreeBefore[fw] = acc;
     }
     __syncthreads();
-    for (int j = lane; j < d; j += 64) {
-        uint64_t* ent = T + static_cast<int64_t>(j) * ES;
-        for (int k = 0; k < hw; ++k) ent[2 + k] = 0;
-        const int k = sSlot[j];
-        if (k < 0) {
-            ent[0] = 0;
-            ent[1] = 0;
-            const int w = j >> 6;
-            const int idx = sFreeBefore[w] + __popcll(sFree[w] & ((1ull << (j & 63)) - 1));
-            ent[2 + (idx >> 6)] |= 1ull << (idx & 63);
-        } else {
-            const uint64_t* row = B + static_cast<int64_t>(k) * W;
-            ent[0] = row[fw];
-            ent[1] = row[fw + 1];
-            for (int w = 0; w < fw; ++w) {
-                uint64_t v = row[w] & sFree[w];
-                while (v) {
-                    const int b = ffs64(v);
-                    v &= v - 1;
-                    const int idx = sFreeBefore[w] + __popcll(sFree[w] & ((1ull << b) - 1));
-                    ent[2 + (idx >> 6)] |= 1ull << (idx & 63);
+    // free columns in ascending order, 64 per pass: row i of the pass is h of the
+    // (i0 + i)-th free column.  Lanes walk the retained rows: a set bit of r_k at a
+    // free column f of the pass puts the pivot of r_k into h_f.
+    for (int i0 = 0; i0 < t; i0 += 64) {
+        const int nrow = (t - i0) < 64 ? (t - i0) : 64;
+        for (int k = lane; k < nrow * fw; k += 64) sH[k / fw][k % fw] = 0;
+        __syncthreads();
+        // unit bit of each free column of the pass
+        for (int w = 0; w < fw; ++w) {
+            uint64_t v = sFree[w];
+            const int base = sFreeBefore[w];
+            if (base + __popcll(v) <= i0 || base >= i0 + nrow) continue;
+            if (lane < 64) {
+                // the lane-th set bit of this word, if it belongs to the pass
+                uint64_t u = v;
+                for (int skip = lane; skip > 0 && u; --skip) u &= u - 1;
+                const int idx = base + lane;
+                if (u && idx >= i0 && idx < i0 + nrow) {
+                    const int f = 64 * w + ffs64(u);
+                    atomicOr(reinterpret_cast<unsigned long long*>(&sH[idx - i0][f >> 6]), 1ull << (f & 63));
                 }
             }
         }
+        for (int k = lane; k < r; k += 64) {
+            const int p = min(max(piv[k], 0), n);
+            const uint64_t* row = B + static_cast<int64_t>(k) * W;
+            for (int w = 0; w < fw; ++w) {
+                const int base = sFreeBefore[w];
+                const uint64_t fr = sFree[w];
+                if (base + __popcll(fr) <= i0 || base >= i0 + nrow) continue;
+                uint64_t v = row[w] & fr;
+                while (v) {
+                    const int b = ffs64(v);
+                    v &= v - 1;
+                    const int idx = base + __popcll(fr & ((1ull << b) - 1));
+                    if (idx >= i0 && idx < i0 + nrow)
+                        atomicOr(reinterpret_cast<unsigned long long*>(&sH[idx - i0][p >> 6]), 1ull << (p & 63));
+                }
+            }
+        }
+        __syncthreads();
+        for (int k = lane; k < nrow * fw; k += 64) H[static_cast<int64_t>(i0) * fw + k] = sH[k / fw][k % fw];
+        __syncthreads();
     }
 }
 
-// encode: one lane per query
+// x words of a query, with bits past the stride read as zero
+template <int SMAX>
+struct QueryX {
+    uint64_t xr[SMAX > 0 ? SMAX : 1];
+    const uint64_t* xq;
+    int S;
+    __device__ __forceinline__ void load(const uint64_t* p, int stride, bool valid) {
+        xq = p;
+        S = stride;
+        if constexpr (SMAX > 0) {
+#pragma unroll
+            for (int k = 0; k < SMAX; ++k) xr[k] = (valid && k < S) ? p[k] : 0ull;
+        }
+    }
+    __device__ __forceinline__ uint64_t word(int w) const {
+        if constexpr (SMAX > 0) {
+            uint64_t v = 0;
+#pragma unroll
+            for (int k = 0; k < SMAX; ++k) v = (w == k) ? xr[k] : v;
+            return v;
+        } else {
+            return w < S ? xq[w] : 0ull;
+        }
+    }
+};
+
+// any x bit at or above the width n: outside the context's ambient space
+template <int SMAX>
+__device__ __forceinline__ bool outside_width(const QueryX<SMAX>& x, int n) {
+    bool outside = false;
+    for (int w = (n >> 6); w < x.S; ++w) {
+        const uint64_t v = x.word(w);
+        const int lo = 64 * w;
+        outside |= (lo >= n) ? (v != 0) : ((v >> (n - lo)) != 0);
+    }
+    return outside;
+}
+
+// even overlap of phi = [x | 1] with every parity-check row of the context
+template <int SMAX>
+__device__ __forceinline__ bool parity_ok(const EncArgs& e, int c, int n, const QueryX<SMAX>& x) {
+    const int fw = feat_words(n), d = n + 1;
+    const int t = d - min(max(e.rank[c], 0), d);
+    const uint64_t* H = e.tables + e.basis_off[c];
+    const int cw = n >> 6;
+    const uint64_t cbit = 1ull << (n & 63);
+    for (int f = 0; f < t; ++f) {
+        const uint64_t* h = H + static_cast<int64_t>(f) * fw;
+        uint64_t acc = 0;
+        for (int w = 0; w < fw; ++w) {
+            uint64_t qw = x.word(w);
+            if (w == cw) qw |= cbit;
+            acc ^= h[w] & qw;
+        }
+        if (__popcll(acc) & 1) return false;
+    }
+    return true;
+}
+
+// per-lane encode by gathering the map columns of the set bits (lanes may hold different contexts)
+template <int SMAX>
+__device__ __forceinline__ bool encode_gather(const EncArgs& e, int c, const QueryX<SMAX>& x, uint64_t& z0,
+                                              uint64_t& z1) {
+    const int n = e.n_bits[c];
+    const int fw = feat_words(n);
+    if (outside_width(x, n)) return false;
+    const uint64_t* M = e.maps + e.map_off[c];
+    const uint64_t* Z = e.tables + e.zero_word;
+    z0 = M[2 * n];  // constant column: always set
+    z1 = M[2 * n + 1];
+    const int xw = x.S < fw ? x.S : fw;
+    for (int w = 0; w < xw; ++w) {
+        const uint64_t v = x.word(w);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            uint32_t u = h ? static_cast<uint32_t>(v >> 32) : static_cast<uint32_t>(v);
+            const uint64_t* Mh = M + 2 * (64 * w + 32 * h);
+            while (u) {  // four gathers in flight; missing ones read a zero column
+                const uint64_t* p0 = Mh + 2 * __builtin_ctz(u);
+                u &= u - 1;
+                const uint64_t* p1 = u ? Mh + 2 * __builtin_ctz(u) : Z;
+                u &= u - 1;
+                const uint64_t* p2 = u ? Mh + 2 * __builtin_ctz(u) : Z;
+                u &= u - 1;
+                const uint64_t* p3 = u ? Mh + 2 * __builtin_ctz(u) : Z;
+                u &= u - 1;
+                const ulonglong2 a0 = *reinterpret_cast<const ulonglong2*>(p0);
+                const ulonglong2 a1 = *reinterpret_cast<const ulonglong2*>(p1);
+                const ulonglong2 a2 = *reinterpret_cast<const ulonglong2*>(p2);
+                const ulonglong2 a3 = *reinterpret_cast<const ulonglong2*>(p3);
+                z0 ^= a0.x ^ a1.x ^ a2.x ^ a3.x;
+                z1 ^= a0.y ^ a1.y ^ a2.y ^ a3.y;
+            }
+        }
+    }
+    return parity_ok(e, c, n, x);
+}
+
+// one lane per query, queries in arbitrary order
 __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs e) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
     if (q >= e.nq) return;
@@ -605,77 +1002,32 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs e) {
         fl = F2_Q_BAD_CTX;
     } else {
         if (e.ctx_flags[c] & F2_CTX_CONTRADICTION) fl = F2_Q_CTX_CONTRADICTORY;
-        const int n = e.n_bits[c];
-        const int fw = feat_words(n), d = n + 1;
-        const int hw = (d - min(max(e.rank[c], 0), d) + 63) >> 6, ES = 2 + hw;
-        const uint64_t* T = e.tables + e.basis_off[c];
-        const uint64_t* xq = e.x + q * e.stride;
-        bool outside = false;
-        for (int w = 0; w < e.stride; ++w) {
-            const int lo = 64 * w;
-            const uint64_t v = xq[w];
-            if (lo >= n) outside |= (v != 0);
-            else if (n - lo < 64) outside |= (v >> (n - lo)) != 0;
-        }
-        if (outside) {
-            fl |= F2_Q_OUT_OF_SPAN;
+        bool in;
+        if (e.stride <= 4) {
+            QueryX<4> x;
+            x.load(e.x + q * e.stride, e.stride, true);
+            in = encode_gather(e, c, x, z0, z1);
         } else {
-            bool inspan = true;
-            const int xw = e.stride < fw ? e.stride : fw;
-            for (int h0 = 0; h0 < (hw > 0 ? hw : 1); h0 += kEncHW) {
-                uint64_t h[kEncHW];
-#pragma unroll
-                for (int k = 0; k < kEncHW; ++k) h[k] = 0;
-                const bool first = (h0 == 0);
-                const int hn = (hw - h0) < kEncHW ? (hw - h0) : kEncHW;
-                // constant feature (storage bit n) is always set
-                {
-                    const uint64_t* ent = T + static_cast<int64_t>(n) * ES;
-                    if (first) {
-                        z0 ^= ent[0];
-                        z1 ^= ent[1];
-                    }
-#pragma unroll
-                    for (int k = 0; k < kEncHW; ++k)
-                        if (k < hn) h[k] ^= ent[2 + h0 + k];
-                }
-                for (int w = 0; w < xw; ++w) {
-                    uint64_t v = xq[w];
-                    while (v) {
-                        const int j = 64 * w + ffs64(v);
-                        v &= v - 1;
-                        const uint64_t* ent = T + static_cast<int64_t>(j) * ES;
-                        if (first) {
-                            z0 ^= ent[0];
-                            z1 ^= ent[1];
-                        }
-#pragma unroll
-                        for (int k = 0; k < kEncHW; ++k)
-                            if (k < hn) h[k] ^= ent[2 + h0 + k];
-                    }
-                }
-#pragma unroll
-                for (int k = 0; k < kEncHW; ++k) inspan &= (h[k] == 0);
-            }
-            if (!inspan) {
-                fl |= F2_Q_OUT_OF_SPAN;
-                z0 = z1 = 0;
-            }
+            QueryX<0> x;
+            x.load(e.x + q * e.stride, e.stride, true);
+            in = encode_gather(e, c, x, z0, z1);
+        }
+        if (!in) {
+            fl |= F2_Q_OUT_OF_SPAN;
+            z0 = z1 = 0;
         }
     }
-    if (fl & (F2_Q_BAD_CTX | F2_Q_OUT_OF_SPAN)) z0 = z1 = 0;
-    e.words[2 * q] = z0;
-    e.words[2 * q + 1] = z1;
+    ulonglong2 out;
+    out.x = z0;
+    out.y = z1;
+    *reinterpret_cast<ulonglong2*>(e.words + 2 * q) = out;
     e.qflags[q] = fl;
 }
 
 inline size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
-int grid_for_class(int cls, int num_ctx) {
-    static const int caps[kClasses] = {4096, 4096, 2048, 1024, 512};
-    int g = caps[cls];
-    return num_ctx < g ? (num_ctx > 0 ? num_ctx : 1) : g;
-}
+// workgroups of a fit kernel: at most one per context, at most `cap`
+unsigned fit_grid(int num_ctx, int cap) { return static_cast<unsigned>(num_ctx < cap ? num_ctx : cap); }
 
 }  // namespace
 
@@ -717,7 +1069,7 @@ int f2_fit_layout(const int32_t* n_bits_host, int32_t num_ctx, int64_t* basis_of
 
 size_t f2_fit_workspace_bytes(int32_t num_ctx) {
     if (num_ctx < 0) return 0;
-    return 256 + align256(sizeof(int32_t) * static_cast<size_t>(kClasses) * static_cast<size_t>(num_ctx));
+    return 256;  // reserved; the current kernels keep all scratch on chip
 }
 
 int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m,
@@ -752,21 +1104,14 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     a.ctx_flags = m->ctx_flags;
     a.n_contra = m->n_contra;
     a.first_contra = m->first_contra_row;
-    a.counters = static_cast<int32_t*>(workspace);
-    a.lists = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + 256);
-
-    hipLaunchKernelGGL(k_fit_init, dim3(1), dim3(64), 0, s, a.counters);
-    hipLaunchKernelGGL(k_fit_plan, dim3((C + 255) / 256), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_fit_small<1>, dim3(grid_for_class(0, C)), dim3(64), 0, s, a, 0);
-    hipLaunchKernelGGL(k_fit_small<2>, dim3(grid_for_class(1, C)), dim3(64), 0, s, a, 1);
-    hipLaunchKernelGGL(k_fit_small<4>, dim3(grid_for_class(2, C)), dim3(64), 0, s, a, 2);
-    hipLaunchKernelGGL(k_fit_small<8>, dim3(grid_for_class(3, C)), dim3(64), 0, s, a, 3);
-    hipLaunchKernelGGL(k_fit_large, dim3(grid_for_class(4, C)), dim3(kLargeThreads), 0, s, a, 4);
+    hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid(C, 8192)), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_fit_lds, dim3(fit_grid(C, 1024)), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_fit_large, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 
-size_t f2_encode_workspace_bytes(const f2_model* m) {
-    if (!m || m->basis_words < 0) return 0;
+size_t f2_encode_workspace_bytes(const f2_model* m, int64_t num_queries) {
+    if (!m || m->basis_words < 0 || m->num_ctx < 0 || num_queries < 0) return 0;
     return align256(sizeof(uint64_t) * static_cast<size_t>(m->basis_words)) + 256;
 }
 
@@ -776,10 +1121,10 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     if (!m || m->num_ctx < 0 || num_queries < 0 || x_stride_words < 1) return F2_EINVAL;
     if (num_queries == 0) return F2_OK;
     if (!ctx_id || !x || !words_out || !qflags_out) return F2_EINVAL;
-    if (m->num_ctx > 0 && (!m->n_bits || !m->basis_off || !m->piv_off || !m->basis || !m->pivots || !m->rank ||
-                           !m->ctx_flags))
+    if (m->num_ctx > 0 && (!m->n_bits || !m->basis_off || !m->piv_off || !m->map_off || !m->basis || !m->pivots ||
+                           !m->maps || !m->rank || !m->ctx_flags))
         return F2_EINVAL;
-    if (!workspace || workspace_bytes < f2_encode_workspace_bytes(m) ||
+    if (!workspace || workspace_bytes < f2_encode_workspace_bytes(m, num_queries) ||
         (reinterpret_cast<uintptr_t>(workspace) & 255u))
         return F2_EWORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -792,16 +1137,19 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     e.pivots = m->pivots;
     e.rank = m->rank;
     e.ctx_flags = m->ctx_flags;
+    e.map_off = m->map_off;
+    e.maps = m->maps;
     e.tables = static_cast<uint64_t*>(workspace);
+    e.zero_word = static_cast<int64_t>(align256(sizeof(uint64_t) * static_cast<size_t>(m->basis_words)) / 8);
     e.ctx_id = ctx_id;
     e.x = x;
     e.stride = x_stride_words;
     e.nq = num_queries;
     e.words = words_out;
     e.qflags = qflags_out;
-    if (m->num_ctx > 0) hipLaunchKernelGGL(k_enc_prepare, dim3(m->num_ctx), dim3(64), 0, s, e);
     const int64_t blocks = (num_queries + kEncThreads - 1) / kEncThreads;
     if (blocks > 0x7fffffff) return F2_EINVAL;
+    hipLaunchKernelGGL(k_enc_prepare, dim3(m->num_ctx > 0 ? m->num_ctx : 1), dim3(64), 0, s, e);
     hipLaunchKernelGGL(k_encode, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }

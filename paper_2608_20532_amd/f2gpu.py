@@ -60,7 +60,7 @@ def _load():
     L.f2_fit_workspace_bytes.restype = sz
     L.f2_fit_batch.argtypes = [P, i64, P, MP, P, sz, P]
     L.f2_fit_batch.restype = ctypes.c_int
-    L.f2_encode_workspace_bytes.argtypes = [MP]
+    L.f2_encode_workspace_bytes.argtypes = [MP, i64]
     L.f2_encode_workspace_bytes.restype = sz
     L.f2_encode_batch.argtypes = [MP, P, P, i32, i64, P, P, P, sz, P]
     L.f2_encode_batch.restype = ctypes.c_int
@@ -106,8 +106,8 @@ def f2_fit_workspace_bytes(num_ctx: int) -> int:
     return int(lib.f2_fit_workspace_bytes(num_ctx))
 
 
-def f2_encode_workspace_bytes(model: "Model") -> int:
-    return int(lib.f2_encode_workspace_bytes(ctypes.byref(model.struct())))
+def f2_encode_workspace_bytes(model: "Model", num_queries: int) -> int:
+    return int(lib.f2_encode_workspace_bytes(ctypes.byref(model.struct()), int(num_queries)))
 
 
 class Model:
@@ -182,7 +182,7 @@ def encode(model: Model, ctx_dev, x_dev, stride: int, stream=None):
     Q = int(ctx_dev.numel())
     words = torch.empty((max(Q, 1), 2), dtype=torch.int64, device=ctx_dev.device)
     qf = torch.empty(max(Q, 1), dtype=torch.uint8, device=ctx_dev.device)
-    nb = f2_encode_workspace_bytes(model)
+    nb = f2_encode_workspace_bytes(model, Q)
     ws = workspace(nb, ctx_dev.device)
     _check(f2_encode_batch(model, ctx_dev, x_dev, stride, Q, words, qf, ws, nb, stream), "f2_encode_batch")
     return words[:Q], qf[:Q]

@@ -1,0 +1,76 @@
+"""Host-side checks of the C-ABI library (no GPU needed): it loads, exports every
+entry point include/f2gpu.h declares, and its host helpers follow the documented
+layout and argument rules."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "f2gpu.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(f2_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2608_20532_amd import f2gpu
+    names = declared_functions()
+    assert len(names) >= 6
+    L = ctypes.CDLL(f2gpu.LIB_PATH)
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(f2gpu.EXPORTS) == set(names)
+
+
+def test_layout_matches_documented_capacities():
+    from paper_2608_20532_amd import f2gpu
+    n = np.array([0, 1, 62, 63, 64, 127, 128, 4095, 33], np.int32)
+    got = f2gpu.f2_fit_layout(n)
+    want = oracle.layout(n)   # the oracle's own copy of the documented rule
+    for g, w in zip(got, want):
+        assert np.array_equal(g, w)
+
+
+def test_layout_errors():
+    from paper_2608_20532_amd import f2gpu
+    with pytest.raises(RuntimeError, match="F2_MAX_N_BITS|above"):
+        f2gpu.f2_fit_layout(np.array([4096], np.int32))
+    with pytest.raises(RuntimeError, match="invalid"):
+        f2gpu.f2_fit_layout(np.array([-1], np.int32))
+    assert f2gpu.f2_fit_layout(np.zeros(0, np.int32))[0].tolist() == [0]
+
+
+def test_status_strings_and_workspace_sizes():
+    from paper_2608_20532_amd import f2gpu
+    for st in (0, -1, -2, -3, -4):
+        assert f2gpu.f2_status_string(st) != "unknown status"
+    assert f2gpu.f2_status_string(7) == "unknown status"
+    assert f2gpu.f2_fit_workspace_bytes(10) >= 1 and f2gpu.f2_fit_workspace_bytes(-1) == 0
+    m = f2gpu.f2_model()
+    m.num_ctx, m.basis_words = 10, 1000
+    small = f2gpu.lib.f2_encode_workspace_bytes(ctypes.byref(m), 1000)
+    big = f2gpu.lib.f2_encode_workspace_bytes(ctypes.byref(m), 1 << 20)
+    assert small >= 8000 and big >= small   # parity rows live within the basis capacity
+
+
+def test_calls_with_bad_host_arguments_enqueue_nothing():
+    """Argument errors are returned before any device work (so these run without a GPU)."""
+    from paper_2608_20532_amd import f2gpu
+    L = f2gpu.lib
+    assert L.f2_fit_batch(None, 0, None, None, None, 0, None) == f2gpu.F2_EINVAL
+    m = f2gpu.f2_model()
+    m.num_ctx = -1
+    assert L.f2_fit_batch(None, 0, None, ctypes.byref(m), None, 0, None) == f2gpu.F2_EINVAL
+    m.num_ctx = 0
+    assert L.f2_fit_batch(None, 0, None, ctypes.byref(m), None, 0, None) == f2gpu.F2_OK   # nothing to do
+    assert L.f2_encode_batch(ctypes.byref(m), None, None, 0, 5, None, None, None, 0, None) == f2gpu.F2_EINVAL
+    assert L.f2_encode_batch(ctypes.byref(m), None, None, 1, 0, None, None, None, 0, None) == f2gpu.F2_OK
+    m.num_ctx = 3
+    assert L.f2_fit_batch(None, 0, None, ctypes.byref(m), None, 0, None) == f2gpu.F2_EINVAL

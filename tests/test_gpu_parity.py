@@ -226,3 +226,42 @@ def test_encode_recipe5_full_size_sampled(f2):
     sample = np.sort(np.random.default_rng(1).choice(nq, size=200_000, replace=False))
     planted = _encode_and_compare(f2, wl, model, ref, nq, stride, frac, zipf, sample=sample)
     assert 0.008 < planted.mean() < 0.012
+
+
+def test_encode_grouped_path_random_widths(f2):
+    """A batch large enough for the context-grouped encode, with every context class and bad ids mixed in."""
+    rng = np.random.default_rng(21)
+    widths = list(rng.integers(0, 190, size=300)) + list(rng.integers(190, 600, size=30)) + [0, 63, 64, 4095]
+    wl = _random_batch(23, widths, max_rows=100)
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    stride = 3
+    nq = 150_000
+    ctx = rng.integers(-3, wl.num_ctx + 3, size=nq).astype(np.int32)
+    x = np.zeros((nq, stride), np.uint64)
+    ok = (ctx >= 0) & (ctx < wl.num_ctx)
+    # half the queries: the x of a training row with the constant set (in span when the width fits
+    # the stride), half random junk
+    for i in np.nonzero(ok)[0][: nq // 2]:
+        c = int(ctx[i]); n = int(wl.n_bits[c]); fw = (n + 64) // 64; m = int(wl.m_rows[c])
+        if m == 0:
+            continue
+        rows_c = wl.rows[wl.row_off[c]:wl.row_off[c + 1]].reshape(-1, fw + 2)
+        affine = np.nonzero((rows_c[:, n // 64] >> np.uint64(n % 64)) & np.uint64(1))[0]
+        if len(affine) == 0:
+            continue
+        row = rows_c[affine[int(rng.integers(0, len(affine)))]]
+        k = min(stride, fw)
+        x[i, :k] = row[:k]
+        for w in range(k):  # keep only x_0 .. x_{n-1}: drop the constant and the row's padding bits
+            lo = 64 * w
+            if n - lo < 64:
+                x[i, w] &= np.uint64((1 << max(n - lo, 0)) - 1)
+    junk = np.nonzero(ok)[0][nq // 2:]
+    x[junk] = rng.integers(0, 2 ** 63, size=(len(junk), stride), dtype=np.uint64) & np.uint64(0xFF)
+    words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x.reshape(-1)), stride)
+    import torch
+    torch.cuda.synchronize()
+    rw, rq = oracle.encode_batch(ref, ctx, x.reshape(-1), stride)
+    parity.compare_encode(words, qf, rw, rq)
+    assert (rq == 0).sum() > 1000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 1000 and (rq & oracle.Q_BAD_CTX).any()
