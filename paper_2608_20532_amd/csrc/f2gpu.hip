@@ -33,7 +33,7 @@
 namespace {
 
 constexpr int kLargeRows = 64;       // rows per block, large path
-constexpr int kLargeThreads = 256;
+constexpr int kLargeThreads = 512;
 constexpr int kMaxW = 66;            // widest row: 64 feature words + 2 output words
 constexpr int kEncThreads = 256;
 
@@ -591,21 +591,64 @@ __global__ __launch_bounds__(64) void k_fit_lds(FitArgs a) {
     }
 }
 // ---------------------------------------------------------------------------
-// large-context fit: one workgroup of 4 wavefronts per context.  The working
-// basis lives in the caller's basis buffer, one slot per priority position
-// (slot t holds the row whose pivot is the t-th highest-priority feature), so
-// that the final descending-priority order is an in-place compaction.
+// large-context fit (fw > 8): one workgroup of 8 wavefronts per context, the
+// lanes of a wavefront spanning the words of a row.  The working basis lives in
+// the caller's basis buffer, one slot per priority position (slot t holds the
+// row whose pivot is the t-th highest-priority feature), so that the final
+// descending-priority order is an in-place compaction.  Rows go in blocks of 64:
+//   (1) block reduce: each wavefront reduces 8 rows of the block against every
+//       retained row; the selection bits are the rows' unreduced bits at the
+//       pivot columns (the basis is fully reduced), read a pivot word at a time;
+//   (2) in-block elimination in stream order;
+//   (3) the block's new rows are fully reduced among themselves;
+//   (4) the new pivots are cleared from the retained rows; (5) insertion.
+// Once the rank reaches d every later row lies in the span and the basis is the
+// identity on the features, so a row's residual is y + M phi (the canonical
+// map, staged in LDS): those rows are only checked for contradictions.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int prio_slot(int p, int n) { return p < n ? n - 1 - p : n; }
 __device__ __forceinline__ int slot_pivot(int t, int n) { return t < n ? n - 1 - t : n; }
 
+constexpr int kLargeWaves = kLargeThreads / 64;
+constexpr int kRowsPerWave = kLargeRows / kLargeWaves;
+constexpr int kMaxD = F2_MAX_N_BITS + 1;
+
+// Stage the retained rows whose pivots are the set bits of pivot word pw into
+// dst[0 .. popc): wavefront v copies the rows of bits v, v+8, ... (lanes over
+// words); a row's staging index is the number of set bits below its bit.
+__device__ __forceinline__ void stage_rows(uint64_t (*dst)[kMaxW], const uint64_t* B, uint64_t pmw, int pw, int n,
+                                           int W, int wave, int lane) {
+    for (int b = wave; b < 64; b += kLargeWaves) {
+        if (!((pmw >> b) & 1ull)) continue;
+        const int r = __popcll(pmw & ((1ull << b) - 1));
+        const uint64_t* src = B + static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W;
+        if (lane < W) dst[r][lane] = src[lane];
+        if (64 + lane < W) dst[r][64 + lane] = src[64 + lane];
+    }
+}
+
+__device__ __forceinline__ void unstage_rows(const uint64_t (*src)[kMaxW], uint64_t* B, uint64_t pmw, int pw, int n,
+                                             int W, int wave, int lane) {
+    for (int b = wave; b < 64; b += kLargeWaves) {
+        if (!((pmw >> b) & 1ull)) continue;
+        const int r = __popcll(pmw & ((1ull << b) - 1));
+        uint64_t* dst = B + static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W;
+        if (lane < W) dst[lane] = src[r][lane];
+        if (64 + lane < W) dst[64 + lane] = src[r][64 + lane];
+    }
+}
+
 __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
     __shared__ uint64_t sRow[kLargeRows][kMaxW];
+    // one buffer, two uses: two halves of staged retained rows (blocked phase), map columns (full-rank phase)
+    __shared__ uint64_t sBuf[2 * kLargeRows * kMaxW];
+    uint64_t (*sZ)[2] = reinterpret_cast<uint64_t (*)[2]>(sBuf);
     __shared__ uint64_t sPmask[64];
+    __shared__ uint64_t sNew[kLargeRows][kMaxW];  // the block's new rows, in insertion order
     __shared__ int sNewRow[kLargeRows];  // block row of the k-th new pivot
     __shared__ int sNewPiv[kLargeRows];  // its pivot
-    __shared__ int sP, sNumNew, sContra;
-    __shared__ long long sFirst;
+    __shared__ int sNumNew, sContra;
+    __shared__ long long sFirst, sFirstCons;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
     for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
@@ -630,10 +673,13 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
         if (tid == 0) {
             sContra = 0;
             sFirst = -1;
+            sFirstCons = 0x7fffffffffffffffll;
         }
         __syncthreads();
+        int rank = 0;
 
-        for (int64_t b0 = 0; b0 < m; b0 += kLargeRows) {
+        int64_t b0 = 0;
+        for (; b0 < m && rank < d; b0 += kLargeRows) {
             const int nb = static_cast<int>((m - b0) < kLargeRows ? (m - b0) : kLargeRows);
             for (int k = tid; k < nb * W; k += kLargeThreads) {
                 const int r = k / W, w = k - r * W;
@@ -644,31 +690,80 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
             if (tid == 0) sNumNew = 0;
             __syncthreads();
 
-            // (1) block reduce against the retained basis, lanes over words
-            for (int r = wave; r < nb; r += 4) {
-                uint64_t acc0 = 0, acc1 = 0;
-                for (int w = 0; w < fw; ++w) {
-                    uint64_t v = sRow[r][w] & sPmask[w];
-                    while (v) {
-                        const int p = 64 * w + ffs64(v);
-                        v &= v - 1;
-                        const uint64_t* src = B + static_cast<int64_t>(prio_slot(p, n)) * W;
-                        if (lane < W) acc0 ^= src[lane];
-                        if (64 + lane < W) acc1 ^= src[64 + lane];
-                    }
+            // (1) block reduce against the retained basis
+            if (rank > 0) {
+                uint64_t acc[kRowsPerWave], acc2[kRowsPerWave], orig[kRowsPerWave];
+#pragma unroll
+                for (int r = 0; r < kRowsPerWave; ++r) {
+                    const int i = wave + kLargeWaves * r;
+                    acc[r] = (i < nb && lane < W) ? sRow[i][lane] : 0ull;
+                    acc2[r] = (i < nb && 64 + lane < W) ? sRow[i][64 + lane] : 0ull;
+                    orig[r] = acc[r];
                 }
-                if (lane < W) sRow[r][lane] ^= acc0;
-                if (64 + lane < W) sRow[r][64 + lane] ^= acc1;
+                // pivot words in order, staged two at a time: the next word loads while this one is used
+                int pw = 0;
+                while (pw < fw && !sPmask[pw]) ++pw;
+                int half = 0;
+                if (pw < fw) stage_rows(reinterpret_cast<uint64_t (*)[kMaxW]>(sBuf), B, sPmask[pw], pw, n, W, wave, lane);
+                __syncthreads();
+                while (pw < fw) {
+                    int nx = pw + 1;
+                    while (nx < fw && !sPmask[nx]) ++nx;
+                    uint64_t (*cur)[kMaxW] = reinterpret_cast<uint64_t (*)[kMaxW]>(sBuf + half * kLargeRows * kMaxW);
+                    uint64_t (*nxt)[kMaxW] = reinterpret_cast<uint64_t (*)[kMaxW]>(sBuf + (half ^ 1) * kLargeRows * kMaxW);
+                    if (nx < fw) stage_rows(nxt, B, sPmask[nx], nx, n, W, wave, lane);
+                    const uint64_t pmw = sPmask[pw];
+                    const int cnt = __popcll(pmw);
+                    uint64_t ow[kRowsPerWave];  // pivot word pw of each unreduced row (wavefront-uniform)
+#pragma unroll
+                    for (int r = 0; r < kRowsPerWave; ++r) ow[r] = readlane64(orig[r], pw);
+                    uint64_t rest = pmw;
+                    for (int q0 = 0; q0 < cnt; q0 += 4) {
+                        int bb[4];
+                        uint64_t bv[4], bv2[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {  // issue the four staged reads before using them
+                            const int q = q0 + u < cnt ? q0 + u : q0;
+                            bb[u] = (q0 + u < cnt) ? ffs64(rest) : 64;
+                            rest &= rest - 1;
+                            bv[u] = (lane < W) ? cur[q][lane] : 0ull;
+                            bv2[u] = (64 + lane < W) ? cur[q][64 + lane] : 0ull;
+                        }
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+#pragma unroll
+                            for (int r = 0; r < kRowsPerWave; ++r) {
+                                const uint32_t mk =
+                                    bb[u] < 64 ? static_cast<uint32_t>(0u - static_cast<uint32_t>((ow[r] >> bb[u]) & 1ull)) : 0u;
+                                acc[r] = xor_and(acc[r], mk, bv[u]);
+                                acc2[r] = xor_and(acc2[r], mk, bv2[u]);
+                            }
+                        }
+                    }
+                    __syncthreads();
+                    pw = nx;
+                    half ^= 1;
+                }
+#pragma unroll
+                for (int r = 0; r < kRowsPerWave; ++r) {
+                    const int i = wave + kLargeWaves * r;
+                    if (i < nb && lane < W) sRow[i][lane] = acc[r];
+                    if (i < nb && 64 + lane < W) sRow[i][64 + lane] = acc2[r];
+                }
+                __syncthreads();
             }
-            __syncthreads();
 
-            // (2) in-block elimination in stream order
-            for (int j = 0; j < nb; ++j) {
-                if (wave == 0) {
+            // (2)+(3) in-block elimination in stream order, then the new rows are fully
+            //         reduced among themselves; one wavefront, lanes over words
+            if (wave == 0) {
+                int numNew = 0, ncon = 0;
+                long long firstc = -1;
+                for (int j = 0; j < nb; ++j) {
+                    __builtin_amdgcn_wave_barrier();  // LDS rows written by other lanes above are read below
                     const uint64_t v = (lane < fw) ? sRow[j][lane] : 0ull;
                     const uint64_t vx = (lane == cw) ? (v & ~cbit) : v;
-                    const uint64_t nzm = __ballot(v != 0);
                     const uint64_t nxm = __ballot(vx != 0);
+                    const uint64_t nzm = __ballot(v != 0);
                     int p = -1;
                     if (nxm) {
                         const int top = msb64(nxm);
@@ -676,80 +771,165 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
                     } else if (nzm) {
                         p = n;
                     }
+                    if (p < 0) {  // zero features: redundant, or contradictory with a nonzero output
+                        const bool ynz = (lane == fw || lane == fw + 1) && sRow[j][lane] != 0;
+                        if (__ballot(ynz)) {
+                            if (ncon == 0) firstc = b0 + j;
+                            ++ncon;
+                        }
+                        continue;
+                    }
                     if (lane == 0) {
-                        sP = p;
-                        if (p < 0 && (sRow[j][fw] | sRow[j][fw + 1])) {
-                            if (sContra == 0) sFirst = b0 + j;
-                            ++sContra;
+                        sNewRow[numNew] = j;
+                        sNewPiv[numNew] = p;
+                    }
+                    ++numNew;
+                    // later rows holding bit p: one gather of that column, lane = row
+                    const int r = j + 1 + lane;
+                    uint64_t sel = __ballot(r < nb && ((sRow[r < nb ? r : j][p >> 6] >> (p & 63)) & 1ull));
+                    const uint64_t rj0 = (lane < W) ? sRow[j][lane] : 0ull;
+                    const uint64_t rj1 = (64 + lane < W) ? sRow[j][64 + lane] : 0ull;
+                    while (sel) {  // eight rows at a time: all reads, then all writes
+                        int rr[8];
+                        uint64_t t0[8], t1[8];
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) {
+                            rr[u] = sel ? j + 1 + ffs64(sel) : -1;
+                            sel &= sel - 1;
+                            const int rs = rr[u] < 0 ? j : rr[u];
+                            t0[u] = (lane < W) ? sRow[rs][lane] : 0ull;
+                            t1[u] = (64 + lane < W) ? sRow[rs][64 + lane] : 0ull;
                         }
-                        if (p >= 0) {
-                            sNewRow[sNumNew] = j;
-                            sNewPiv[sNumNew] = p;
-                            ++sNumNew;
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) {
+                            if (rr[u] < 0) continue;
+                            if (lane < W) sRow[rr[u]][lane] = t0[u] ^ rj0;
+                            if (64 + lane < W) sRow[rr[u]][64 + lane] = t1[u] ^ rj1;
                         }
                     }
                 }
-                __syncthreads();
-                const int p = sP;
-                if (p >= 0) {
-                    for (int r = j + 1 + wave; r < nb; r += 4) {
-                        if ((sRow[r][p >> 6] >> (p & 63)) & 1ull) {
-                            if (lane < W) sRow[r][lane] ^= sRow[j][lane];
-                            if (64 + lane < W) sRow[r][64 + lane] ^= sRow[j][64 + lane];
+                for (int k = numNew - 1; k > 0; --k) {  // latest pivot first
+                    __builtin_amdgcn_wave_barrier();
+                    const int jk = sNewRow[k], pk = sNewPiv[k];
+                    uint64_t sel = __ballot(lane < k && ((sRow[sNewRow[lane < k ? lane : 0]][pk >> 6] >> (pk & 63)) & 1ull));
+                    const uint64_t rk0 = (lane < W) ? sRow[jk][lane] : 0ull;
+                    const uint64_t rk1 = (64 + lane < W) ? sRow[jk][64 + lane] : 0ull;
+                    while (sel) {  // eight rows at a time: all reads, then all writes
+                        int je[8];
+                        uint64_t t0[8], t1[8];
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) {
+                            je[u] = sel ? sNewRow[ffs64(sel)] : -1;
+                            sel &= sel - 1;
+                            const int rs = je[u] < 0 ? jk : je[u];
+                            t0[u] = (lane < W) ? sRow[rs][lane] : 0ull;
+                            t1[u] = (64 + lane < W) ? sRow[rs][64 + lane] : 0ull;
+                        }
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) {
+                            if (je[u] < 0) continue;
+                            if (lane < W) sRow[je[u]][lane] = t0[u] ^ rk0;
+                            if (64 + lane < W) sRow[je[u]][64 + lane] = t1[u] ^ rk1;
                         }
                     }
                 }
-                __syncthreads();
+                __builtin_amdgcn_wave_barrier();
+                for (int k = 0; k < numNew; ++k) {  // compact copy for the back-substitution and insertion
+                    const int jk = sNewRow[k];
+                    if (lane < W) sNew[k][lane] = sRow[jk][lane];
+                    if (64 + lane < W) sNew[k][64 + lane] = sRow[jk][64 + lane];
+                }
+                if (lane == 0) {
+                    sNumNew = numNew;
+                    if (ncon) {
+                        if (sContra == 0) sFirst = firstc;
+                        sContra += ncon;
+                    }
+                }
             }
-
-            // (3) fully reduce the new rows among themselves (latest pivot first)
+            __syncthreads();
             const int K = sNumNew;
-            for (int k = K - 1; k > 0; --k) {
-                const int jk = sNewRow[k], pk = sNewPiv[k];
-                for (int e = wave; e < k; e += 4) {
-                    const int je = sNewRow[e];
-                    if ((sRow[je][pk >> 6] >> (pk & 63)) & 1ull) {
-                        if (lane < W) sRow[je][lane] ^= sRow[jk][lane];
-                        if (64 + lane < W) sRow[je][64 + lane] ^= sRow[jk][64 + lane];
-                    }
-                }
-                __syncthreads();
-            }
 
             if (K > 0) {
-                // (4) clear the new pivots from every retained row
-                for (int t = wave; t < d; t += 4) {
-                    const int pt = slot_pivot(t, n);
-                    if (!((sPmask[pt >> 6] >> (pt & 63)) & 1ull)) continue;
-                    uint64_t* row = B + static_cast<int64_t>(t) * W;
-                    uint64_t w0 = (lane < W) ? row[lane] : 0ull;
-                    uint64_t w1 = (64 + lane < W) ? row[64 + lane] : 0ull;
+                // (4) clear the new pivots from every retained row: the retained rows of each
+                //     pivot word are staged in LDS, updated there, and written back
+                for (int pw = 0; pw < fw; ++pw) {
+                    const uint64_t pmw = sPmask[pw];
+                    if (!pmw) continue;
+                    const int cnt = __popcll(pmw);
+                    uint64_t (*sStage)[kMaxW] = reinterpret_cast<uint64_t (*)[kMaxW]>(sBuf);
+                    stage_rows(sStage, B, pmw, pw, n, W, wave, lane);
+                    __syncthreads();
                     const int pk = (lane < K) ? sNewPiv[lane] : 0;
-                    const uint64_t wk = shfl64(w0, pk >> 6);
-                    uint64_t sel = __ballot(lane < K && ((wk >> (pk & 63)) & 1ull));
-                    if (!sel) continue;
-                    while (sel) {
-                        const int k = ffs64(sel);
-                        sel &= sel - 1;
-                        const int jk = sNewRow[k];
-                        if (lane < W) w0 ^= sRow[jk][lane];
-                        if (64 + lane < W) w1 ^= sRow[jk][64 + lane];
+                    for (int q = wave; q < cnt; q += kLargeWaves) {
+                        uint64_t w0 = (lane < W) ? sStage[q][lane] : 0ull;
+                        uint64_t w1 = (64 + lane < W) ? sStage[q][64 + lane] : 0ull;
+                        const uint64_t wk = sStage[q][pk >> 6];
+                        uint64_t sel = __ballot(lane < K && ((wk >> (pk & 63)) & 1ull));
+                        while (sel) {  // eight new rows at a time, reads issued together
+                            uint64_t t0[8], t1[8];
+#pragma unroll
+                            for (int u = 0; u < 8; ++u) {
+                                const int k = sel ? ffs64(sel) : -1;
+                                sel &= sel - 1;
+                                t0[u] = (k >= 0 && lane < W) ? sNew[k < 0 ? 0 : k][lane] : 0ull;
+                                t1[u] = (k >= 0 && 64 + lane < W) ? sNew[k < 0 ? 0 : k][64 + lane] : 0ull;
+                            }
+                            w0 ^= (t0[0] ^ t0[1]) ^ (t0[2] ^ t0[3]) ^ (t0[4] ^ t0[5]) ^ (t0[6] ^ t0[7]);
+                            w1 ^= (t1[0] ^ t1[1]) ^ (t1[2] ^ t1[3]) ^ (t1[4] ^ t1[5]) ^ (t1[6] ^ t1[7]);
+                        }
+                        if (lane < W) sStage[q][lane] = w0;
+                        if (64 + lane < W) sStage[q][64 + lane] = w1;
                     }
-                    if (lane < W) row[lane] = w0;
-                    if (64 + lane < W) row[64 + lane] = w1;
+                    __syncthreads();
+                    unstage_rows(sStage, B, pmw, pw, n, W, wave, lane);
+                    __syncthreads();
                 }
                 // (5) insert the new rows at their priority slots
-                for (int k = wave; k < K; k += 4) {
-                    const int jk = sNewRow[k];
+                for (int k = wave; k < K; k += kLargeWaves) {
                     uint64_t* row = B + static_cast<int64_t>(prio_slot(sNewPiv[k], n)) * W;
-                    if (lane < W) row[lane] = sRow[jk][lane];
-                    if (64 + lane < W) row[64 + lane] = sRow[jk][64 + lane];
+                    if (lane < W) row[lane] = sNew[k][lane];
+                    if (64 + lane < W) row[64 + lane] = sNew[k][64 + lane];
                 }
                 __syncthreads();
                 if (tid == 0)
                     for (int k = 0; k < K; ++k) sPmask[sNewPiv[k] >> 6] |= 1ull << (sNewPiv[k] & 63);
             }
             __syncthreads();
+            rank += K;
+        }
+
+        if (b0 < m) {
+            // full rank: every remaining row lies in the span; its residual is y + M phi
+            for (int j = tid; j < d; j += kLargeThreads) {
+                const uint64_t* row = B + static_cast<int64_t>(prio_slot(j, n)) * W;
+                sZ[j][0] = row[fw];
+                sZ[j][1] = row[fw + 1];
+            }
+            __syncthreads();
+            for (int64_t r0 = b0; r0 < m; r0 += kLargeThreads) {
+                const int64_t i = r0 + tid;
+                if (i < m) {
+                    const uint64_t* row = R + i * W;
+                    uint64_t z0 = row[fw], z1 = row[fw + 1];
+                    for (int w = 0; w < fw; ++w) {
+                        uint64_t v = row[w];
+                        if (w == fw - 1) v &= tmask;
+                        while (v) {
+                            const int jj = 64 * w + ffs64(v);
+                            v &= v - 1;
+                            z0 ^= sZ[jj][0];
+                            z1 ^= sZ[jj][1];
+                        }
+                    }
+                    if (z0 | z1) {
+                        atomicAdd(&sContra, 1);
+                        atomicMin(&sFirstCons, static_cast<long long>(i));
+                    }
+                }
+            }
+            __syncthreads();
+            if (tid == 0 && sFirst < 0 && sFirstCons != 0x7fffffffffffffffll) sFirst = sFirstCons;
         }
 
         // outputs: canonical map from the slots, then compaction into descending priority
@@ -760,10 +940,8 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
             a.maps[mo + 2 * j] = present ? row[fw] : 0ull;
             a.maps[mo + 2 * j + 1] = present ? row[fw + 1] : 0ull;
         }
-        int rank = 0;
-        for (int w = 0; w < fw; ++w) rank += __popcll(sPmask[w]);
         __syncthreads();
-        for (int t0 = 0; t0 < d; t0 += 4) {
+        for (int t0 = 0; t0 < d; t0 += kLargeWaves) {
             const int t = t0 + wave;
             const int pt = t < d ? slot_pivot(t, n) : 0;
             const bool present = t < d && ((sPmask[pt >> 6] >> (pt & 63)) & 1ull);
