@@ -152,7 +152,7 @@ __device__ __forceinline__ CtxDesc readlane_desc(const CtxDesc& v, int t) {
     return ds;
 }
 
-// width class of a valid context: 0 register basis (fw 1-3), 1 LDS basis (fw 4-8), 2 large
+// width class of a valid context: 0 register basis (fw 1-3), 1 pivot-indexed LDS basis (fw 4-8), 2 large
 __device__ __forceinline__ int width_class(int n) {
     const int fw = feat_words(n);
     return fw <= 3 ? 0 : fw <= 8 ? 1 : 2;
@@ -210,6 +210,7 @@ __device__ __forceinline__ uint64_t xor_and(uint64_t f, uint32_t m, uint64_t d) 
 }
 
 constexpr int kRegMaxFW = 3;
+constexpr int kLongRows = 256;  // contexts with more rows take the multi-wavefront kernel
 constexpr int kRecWords = 6;  // LDS record: fw feature words, 2 output words, pivot (<= 6 words)
 
 template <int FW>
@@ -433,7 +434,7 @@ __global__ __launch_bounds__(64) void k_fit_reg(FitArgs a) {
     const int lane = threadIdx.x;
     for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
         const CtxDesc mine = load_desc(a, blockIdx.x + (k0 + lane) * gridDim.x);
-        uint64_t todo = __ballot(mine.c >= 0 && (mine.bad || width_class(mine.n) == 0));
+        uint64_t todo = __ballot(mine.c >= 0 && (mine.bad || (width_class(mine.n) == 0 && mine.m <= kLongRows)));
         while (todo) {
             const int t = ffs64(todo);
             todo &= todo - 1;
@@ -452,144 +453,288 @@ __global__ __launch_bounds__(64) void k_fit_reg(FitArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// LDS-basis fit (fw 4-8): one wavefront per context, retained rows in LDS
+// pivot-indexed LDS-basis fit: retained row of pivot p in record p (fw + 2
+// words), a pivot-column bitmask beside it.  Used with one wavefront for short
+// contexts of 4-8 feature words and with NW wavefronts for long contexts of up
+// to 8 feature words.  With NW > 1 the next NW blocks of 64 rows are reduced
+// in parallel, one per wavefront; the first block (in stream order) that still
+// holds a nonzero feature residual runs the insertion loop in its own
+// wavefront, the blocks before it are only classified, the blocks after it are
+// redone against the grown basis.  Once the basis stops growing every round
+// completes NW blocks.
 // ---------------------------------------------------------------------------
-constexpr int kLdsFW = 8;
+constexpr int kPivMaxFW = 8;
+constexpr int kPivRec = kPivMaxFW + F2_Y_WORDS;  // record words
+constexpr int kPivCap = 64 * kPivMaxFW;          // d <= 512
+constexpr int kPivWaves = 8;
 
-__global__ __launch_bounds__(64) void k_fit_lds(FitArgs a) {
-    constexpr int FW = kLdsFW;
-    constexpr int CAP = 64 * FW;
-    __shared__ uint64_t sBf[FW][CAP];
-    __shared__ uint64_t sBy[2][CAP];
-    __shared__ int16_t sPiv[CAP];
-    __shared__ int16_t sPos[CAP];
-    __shared__ uint64_t sRow[64][FW];  // this lane's block row (kept in LDS: dynamic word index)
-    const int lane = threadIdx.x;
+template <int FW>
+__device__ __forceinline__ uint64_t sel_word(const uint64_t (&f)[FW], int wi) {
+    uint64_t v = f[0];
+#pragma unroll
+    for (int k = 1; k < FW; ++k) v ^= (f[k] ^ f[0]) & (0ull - static_cast<uint64_t>(wi == k));
+    return v;
+}
 
+struct PivShared {
+    uint64_t rec[kPivCap][kPivRec];
+    uint64_t pm[kPivMaxFW];
+    int flag[kPivWaves];
+    int contra;
+    long long first, round_first;
+};
+
+// reduce this wavefront's block rows against the retained basis (one pass: the basis is fully reduced)
+template <int FW>
+__device__ __forceinline__ void piv_reduce(PivShared& S, int fw, uint64_t (&f)[FW], uint64_t& y0, uint64_t& y1) {
+    uint64_t f0[FW];
+#pragma unroll
+    for (int w = 0; w < FW; ++w) f0[w] = f[w];
+    for (int pw = 0; pw < fw; ++pw) {
+        uint64_t pm = S.pm[pw];
+        if (!pm) continue;
+        const uint64_t ow = sel_word<FW>(f0, pw);  // unreduced word pw of this lane's row
+        while (pm) {
+            int bb[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                bb[u] = pm ? ffs64(pm) : -1;
+                pm &= pm - 1;
+            }
+            uint64_t rv[4][FW + 2];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint64_t* rec = S.rec[64 * pw + (bb[u] < 0 ? 0 : bb[u])];
+#pragma unroll
+                for (int w = 0; w < FW + 2; ++w) rv[u][w] = rec[w];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t mk = bb[u] < 0 ? 0u : bit_mask(ow, bb[u]);
+#pragma unroll
+                for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mk, rv[u][w]);
+                y0 = xor_and(y0, mk, rv[u][FW]);
+                y1 = xor_and(y1, mk, rv[u][FW + 1]);
+            }
+        }
+    }
+}
+
+// insertion loop of one block (one wavefront); returns the rank after the block
+template <int FW>
+__device__ int piv_insert(PivShared& S, int n, int d, int fw, int rank, int64_t b0, bool valid, uint64_t (&f)[FW],
+                          uint64_t& y0, uint64_t& y1, int& ncon, long long& firstc) {
+    const int lane = threadIdx.x & 63;
+    const int cw = n >> 6;
+    const uint64_t cbit = 1ull << (n & 63);
+    uint64_t pending = __ballot(valid);
+    while (pending) {
+        __builtin_amdgcn_wave_barrier();
+        uint64_t any = f[0];
+#pragma unroll
+        for (int w = 1; w < FW; ++w) any |= f[w];
+        const uint64_t nz = __ballot(any != 0) & pending;
+        const int j = nz ? ffs64(nz) : 64;
+        const uint64_t before = (j >= 64) ? pending : (pending & ((1ull << j) - 1));
+        if (before) {
+            const uint64_t cm = __ballot((y0 | y1) != 0) & before;
+            if (cm) {
+                if (ncon == 0) firstc = b0 + ffs64(cm);
+                ncon += __popcll(cm);
+            }
+            pending &= ~before;
+        }
+        if (j >= 64) break;
+        uint64_t F[FW];
+#pragma unroll
+        for (int w = 0; w < FW; ++w) F[w] = readlane64(f[w], j);
+        const uint64_t Y0 = readlane64(y0, j), Y1 = readlane64(y1, j);
+        int p = -1;
+#pragma unroll
+        for (int w = FW - 1; w >= 0; --w) {
+            const uint64_t v = (w == cw) ? (F[w] & ~cbit) : F[w];
+            if (p < 0 && v) p = 64 * w + msb64(v);
+        }
+        if (p < 0) p = n;
+        const int pw = p >> 6, pb = p & 63;
+        {  // rows of the block that hold bit p
+            const uint32_t mm = bit_mask(sel_word<FW>(f, pw), pb);
+#pragma unroll
+            for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, F[w]);
+            y0 = xor_and(y0, mm, Y0);
+            y1 = xor_and(y1, mm, Y1);
+        }
+        // clear p from every retained row (record s for each set pivot bit s)
+        for (int s = lane; s < d; s += 64) {
+            if (!((S.pm[s >> 6] >> (s & 63)) & 1ull)) continue;
+            uint64_t* rec = S.rec[s];
+            if ((rec[pw] >> pb) & 1ull) {
+#pragma unroll
+                for (int w = 0; w < FW; ++w) rec[w] ^= F[w];
+                rec[FW] ^= Y0;
+                rec[FW + 1] ^= Y1;
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (lane == 0) {
+            uint64_t* rec = S.rec[p];
+#pragma unroll
+            for (int w = 0; w < FW; ++w) rec[w] = F[w];
+            rec[FW] = Y0;
+            rec[FW + 1] = Y1;
+            S.pm[pw] |= 1ull << pb;
+        }
+        ++rank;
+        pending &= ~(1ull << j);
+    }
+    (void)fw;
+    return rank;
+}
+
+template <int FW, int NW>
+__device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int c = ds.c, n = ds.n, d = n + 1;
+    const int fw = feat_words(n);  // <= FW; records keep FW feature words, then the two output words
+    const int Wr = fw + F2_Y_WORDS;
+    const int64_t m = ds.m;
+    const uint64_t* R = a.rows + ds.row0;
+    const uint64_t tmask = top_mask(n, fw);
+
+    if (tid < kPivMaxFW) S.pm[tid] = 0;
+    if (tid == 0) {
+        S.contra = 0;
+        S.first = -1;
+    }
+    __syncthreads();
+    int rank = 0;
+    int64_t b0 = 0;
+    while (b0 < m) {
+        const int64_t bw = b0 + 64 * wave;  // this wavefront's block
+        const int64_t i = bw + lane;
+        const bool valid = i < m;
+        uint64_t f[FW], y0 = 0, y1 = 0;
+#pragma unroll
+        for (int w = 0; w < FW; ++w) f[w] = 0;
+        if (valid) {  // rows have fw + 2 words (fw <= FW)
+            const uint64_t* row = R + i * Wr;
+#pragma unroll
+            for (int w = 0; w < FW; ++w)
+                if (w < fw) f[w] = row[w];
+            y0 = row[fw];
+            y1 = row[fw + 1];
+#pragma unroll
+            for (int w = 0; w < FW; ++w)
+                if (w == fw - 1) f[w] &= tmask;
+        }
+        if (rank > 0) piv_reduce<FW>(S, fw, f, y0, y1);
+        uint64_t any = f[0];
+#pragma unroll
+        for (int w = 1; w < FW; ++w) any |= f[w];
+        const bool has_nz = __ballot(valid && any != 0) != 0;
+        int wstar;
+        if constexpr (NW > 1) {
+            if (lane == 0) S.flag[wave] = has_nz ? 1 : 0;
+            if (tid == 0) S.round_first = 0x7fffffffffffffffll;
+            __syncthreads();
+            wstar = NW;
+            for (int w = NW - 1; w >= 0; --w)
+                if (S.flag[w]) wstar = w;
+        } else {
+            wstar = has_nz ? 0 : 1;
+        }
+        int ncon = 0;
+        long long firstc = -1;
+        if (wave < wstar) {  // every residual is zero: redundant or contradictory rows
+            const uint64_t cm = __ballot(valid && (y0 | y1) != 0);
+            if (cm) {
+                ncon = __popcll(cm);
+                firstc = bw + ffs64(cm);
+            }
+        } else if (wave == wstar) {
+            rank = piv_insert<FW>(S, n, d, fw, rank, bw, valid, f, y0, y1, ncon, firstc);
+        }
+        if (lane == 0 && ncon) {
+            atomicAdd(&S.contra, ncon);
+            if constexpr (NW > 1) atomicMin(&S.round_first, firstc);
+            else S.round_first = firstc;
+        }
+        if constexpr (NW > 1) {
+            __syncthreads();
+            if (tid == 0 && S.first < 0 && S.round_first != 0x7fffffffffffffffll) S.first = S.round_first;
+            rank = 0;
+            for (int w = 0; w < fw; ++w) rank += __popcll(S.pm[w]);
+            __syncthreads();
+        } else {
+            if (lane == 0 && ncon && S.first < 0) S.first = firstc;
+            __builtin_amdgcn_wave_barrier();
+        }
+        b0 += 64 * static_cast<int64_t>(wstar < NW ? wstar + 1 : NW);
+    }
+    __syncthreads();
+
+    // outputs: basis rows and pivots in descending priority, canonical map, scalars
+    const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
+    const int cw = n >> 6;
+    const uint64_t cbit = 1ull << (n & 63);
+    for (int j = tid; j < d; j += 64 * NW) {
+        const bool present = (S.pm[j >> 6] >> (j & 63)) & 1ull;
+        a.maps[mo + 2 * j] = present ? S.rec[j][FW] : 0ull;
+        a.maps[mo + 2 * j + 1] = present ? S.rec[j][FW + 1] : 0ull;
+        if (!present) continue;
+        int k = rank - 1;
+        if (j != n) {  // pivots of higher priority: x bits above j
+            k = 0;
+            for (int w = j >> 6; w < fw; ++w) {
+                uint64_t v = S.pm[w];
+                if (w == (j >> 6)) v &= (j & 63) == 63 ? 0ull : (~0ull << ((j & 63) + 1));
+                if (w == cw) v &= ~cbit;
+                k += __popcll(v);
+            }
+        }
+        uint64_t* out = a.basis + bo + static_cast<int64_t>(k) * Wr;
+#pragma unroll
+        for (int w = 0; w < FW; ++w)
+            if (w < fw) out[w] = S.rec[j][w];
+        out[fw] = S.rec[j][FW];
+        out[fw + 1] = S.rec[j][FW + 1];
+        a.pivots[po + k] = j;
+    }
+    if (tid == 0) {
+        a.rank[c] = rank;
+        a.n_contra[c] = S.contra;
+        a.first_contra[c] = S.first;
+        a.ctx_flags[c] = S.contra ? F2_CTX_CONTRADICTION : 0u;
+    }
+    __syncthreads();
+}
+
+// width class 1 (fw 4-8, short) with NW = 1; long contexts of fw <= 8 with NW = kPivWaves
+template <int NW>
+__global__ __launch_bounds__(64 * NW) void k_fit_piv(FitArgs a) {
+    __shared__ PivShared S;
+    const int tid = threadIdx.x, lane = tid & 63;
     for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
+        // every wavefront reads the same 64 descriptors, so the ballot is uniform across the workgroup
         const CtxDesc mine = load_desc(a, blockIdx.x + (k0 + lane) * gridDim.x);
-        uint64_t todo = __ballot(mine.c >= 0 && !mine.bad && width_class(mine.n) == 1);
+        const bool take = mine.c >= 0 && !mine.bad && width_class(mine.n) <= 1 &&
+                          (NW > 1 ? mine.m > kLongRows : (mine.m <= kLongRows && width_class(mine.n) == 1));
+        uint64_t todo = __ballot(take);
         while (todo) {
             const int t = ffs64(todo);
             todo &= todo - 1;
             const CtxDesc ds = readlane_desc(mine, t);
-            const int c = ds.c, n = ds.n;
-            const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
-            const int64_t m = ds.m;
-            const uint64_t* R = a.rows + ds.row0;
-            const uint64_t tmask = top_mask(n, fw);
-            const int cw = n >> 6;
-            const uint64_t cbit = 1ull << (n & 63);
-            uint64_t* f = sRow[lane];
-
-            for (int j = lane; j < d; j += 64) sPos[j] = -1;
-            int rank = 0, ncontra = 0;
-            int64_t first = -1;
-            __syncthreads();
-
-            for (int64_t b0 = 0; b0 < m; b0 += 64) {
-                const int64_t i = b0 + lane;
-                const bool valid = i < m;
-                uint64_t y0 = 0, y1 = 0;
-                for (int w = 0; w < FW; ++w) f[w] = 0;
-                if (valid) {
-                    const uint64_t* row = R + i * W;
-                    for (int w = 0; w < fw; ++w) f[w] = row[w];
-                    y0 = row[fw];
-                    y1 = row[fw + 1];
-                    f[fw - 1] &= tmask;
-                }
-                for (int s = 0; s < rank; ++s) {
-                    const int p = sPiv[s];
-                    if ((f[p >> 6] >> (p & 63)) & 1ull) {
-                        for (int w = 0; w < fw; ++w) f[w] ^= sBf[w][s];
-                        y0 ^= sBy[0][s];
-                        y1 ^= sBy[1][s];
-                    }
-                }
-                uint64_t pending = __ballot(valid);
-                while (pending) {
-                    uint64_t any = 0;
-                    for (int w = 0; w < fw; ++w) any |= f[w];
-                    const uint64_t nz = __ballot(any != 0) & pending;
-                    const int j = nz ? ffs64(nz) : 64;
-                    const uint64_t before = (j >= 64) ? pending : (pending & ((1ull << j) - 1));
-                    const uint64_t cm = __ballot((y0 | y1) != 0) & before;
-                    if (cm) {
-                        if (ncontra == 0) first = b0 + ffs64(cm);
-                        ncontra += __popcll(cm);
-                    }
-                    pending &= ~before;
-                    if (j >= 64) break;
-                    __syncthreads();
-                    const uint64_t* Fj = sRow[j];
-                    const uint64_t Y0 = readlane64(y0, j), Y1 = readlane64(y1, j);
-                    int p = -1;
-                    for (int w = fw - 1; w >= 0 && p < 0; --w) {
-                        const uint64_t v = (w == cw) ? (Fj[w] & ~cbit) : Fj[w];
-                        if (v) p = 64 * w + msb64(v);
-                    }
-                    if (p < 0) p = n;
-                    if (lane > j && ((f[p >> 6] >> (p & 63)) & 1ull)) {
-                        for (int w = 0; w < fw; ++w) f[w] ^= Fj[w];
-                        y0 ^= Y0;
-                        y1 ^= Y1;
-                    }
-                    for (int s = lane; s < rank; s += 64) {
-                        if ((sBf[p >> 6][s] >> (p & 63)) & 1ull) {
-                            for (int w = 0; w < fw; ++w) sBf[w][s] ^= Fj[w];
-                            sBy[0][s] ^= Y0;
-                            sBy[1][s] ^= Y1;
-                        }
-                    }
-                    if (lane == 0) {
-                        for (int w = 0; w < fw; ++w) sBf[w][rank] = Fj[w];
-                        for (int w = fw; w < FW; ++w) sBf[w][rank] = 0;
-                        sBy[0][rank] = Y0;
-                        sBy[1][rank] = Y1;
-                        sPiv[rank] = static_cast<int16_t>(p);
-                        sPos[p] = static_cast<int16_t>(rank);
-                    }
-                    ++rank;
-                    pending &= ~(1ull << j);
-                    __syncthreads();
-                }
-                __syncthreads();
+            switch (feat_words(ds.n)) {
+                case 1: fit_ctx_piv<1, NW>(a, ds, S); break;
+                case 2: fit_ctx_piv<2, NW>(a, ds, S); break;
+                case 3: case 4: fit_ctx_piv<4, NW>(a, ds, S); break;
+                default: fit_ctx_piv<8, NW>(a, ds, S); break;
             }
-
-            const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
-            for (int s = lane; s < rank; s += 64) {
-                const int p = sPiv[s];
-                int k = 0;
-                if (p == n) {
-                    k = rank - 1;
-                } else {
-                    for (int t2 = 0; t2 < rank; ++t2) {
-                        const int q = sPiv[t2];
-                        k += (q > p && q < n);
-                    }
-                }
-                uint64_t* out = a.basis + bo + static_cast<int64_t>(k) * W;
-                for (int w = 0; w < fw; ++w) out[w] = sBf[w][s];
-                out[fw] = sBy[0][s];
-                out[fw + 1] = sBy[1][s];
-                a.pivots[po + k] = p;
-            }
-            for (int j = lane; j < d; j += 64) {
-                const int s = sPos[j];
-                a.maps[mo + 2 * j] = s >= 0 ? sBy[0][s] : 0ull;
-                a.maps[mo + 2 * j + 1] = s >= 0 ? sBy[1][s] : 0ull;
-            }
-            if (lane == 0) {
-                a.rank[c] = rank;
-                a.n_contra[c] = ncontra;
-                a.first_contra[c] = first;
-                a.ctx_flags[c] = ncontra ? F2_CTX_CONTRADICTION : 0u;
-            }
-            __syncthreads();
         }
     }
+    (void)tid;
 }
+
 // ---------------------------------------------------------------------------
 // large-context fit (fw > 8): one workgroup of 8 wavefronts per context, the
 // lanes of a wavefront spanning the words of a row.  The working basis lives in
@@ -1283,7 +1428,8 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     a.n_contra = m->n_contra;
     a.first_contra = m->first_contra_row;
     hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid(C, 8192)), dim3(64), 0, s, a);
-    hipLaunchKernelGGL(k_fit_lds, dim3(fit_grid(C, 1024)), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_fit_piv<1>, dim3(fit_grid(C, 1024)), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_fit_piv<kPivWaves>, dim3(fit_grid(C, 1024)), dim3(64 * kPivWaves), 0, s, a);
     hipLaunchKernelGGL(k_fit_large, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }

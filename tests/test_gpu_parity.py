@@ -265,3 +265,38 @@ def test_encode_grouped_path_random_widths(f2):
     rw, rq = oracle.encode_batch(ref, ctx, x.reshape(-1), stride)
     parity.compare_encode(words, qf, rw, rq)
     assert (rq == 0).sum() > 1000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 1000 and (rq & oracle.Q_BAD_CTX).any()
+
+
+def _late_pivot_batch(seed, widths, rows_choices):
+    """Long contexts whose rows first span a small subspace and only later reveal new
+    pivots (one generator added every few hundred rows), with contradictions late."""
+    rng = np.random.default_rng(seed)
+    n_bits, rows_list = [], []
+    for n in widths:
+        n = int(n)
+        fw = (n + 64) // 64
+        d = n + 1
+        m = int(rng.choice(rows_choices))
+        k = int(rng.integers(1, min(d, 40) + 1))
+        pool = rng.integers(0, 2 ** 63, size=(k, fw), dtype=np.uint64) ^ (rng.integers(0, 2, size=(k, fw), dtype=np.uint64) << np.uint64(63))
+        vb = d - 64 * (fw - 1)
+        if vb < 64:
+            pool[:, fw - 1] &= np.uint64((1 << vb) - 1)
+        Wp = rng.integers(0, 2 ** 63, size=(k, 2), dtype=np.uint64)
+        rows = np.zeros((m, fw + 2), np.uint64)
+        for i in range(m):
+            avail = max(1, min(k, 1 + (i * k) // max(1, m)))   # generators unlocked gradually
+            sel = rng.integers(0, 2, size=avail).astype(bool)
+            rows[i, :fw] = np.bitwise_xor.reduce(pool[:avail][sel], axis=0) if sel.any() else 0
+            rows[i, fw:] = np.bitwise_xor.reduce(Wp[:avail][sel], axis=0) if sel.any() else 0
+            if rng.random() < (0.01 if n % 2 else 0.0002):
+                rows[i, fw + int(rng.integers(0, 2))] ^= np.uint64(1) << np.uint64(int(rng.integers(0, 64)))
+        n_bits.append(n)
+        rows_list.append(rows)
+    return synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+
+
+def test_fit_long_contexts_late_pivots(f2):
+    rng = np.random.default_rng(31)
+    widths = [int(w) for w in rng.integers(0, 512, size=40)] + [0, 63, 64, 127, 191, 192, 255, 256, 319, 447, 511]
+    _fit_and_compare(f2, _late_pivot_batch(31, widths, [200, 257, 300, 700, 1500, 2600]))
