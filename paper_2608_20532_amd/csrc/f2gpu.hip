@@ -14,17 +14,18 @@
 //      (its highest-priority feature bit), is broadcast to the later rows that
 //      hold that bit and to the retained rows that hold it (back-substitution
 //      keeps the basis fully reduced), and is inserted.
-// Contexts are sorted into width classes by a plan kernel; each class runs a
-// kernel specialised for its feature-word count, one wavefront per context
-// with the basis in LDS.  Contexts wider than 8 feature words run a
-// workgroup-per-context kernel with the basis in HBM and rows staged in LDS.
+// A plan kernel validates the contexts and sorts them into classes by feature
+// words and length, each class list in decreasing order of estimated work:
+// contexts of up to 3 feature words keep the basis in registers (one lane per
+// retained row), contexts of 4-8 words keep a pivot-indexed basis in LDS (one
+// wavefront, or eight for long contexts, which reduce eight blocks at once),
+// wider contexts run a workgroup-per-context kernel with the basis in HBM and
+// the rows it needs staged in LDS.
 //
-// Encode (Sec. 2.3): a prepare kernel turns each fitted basis into a
-// per-column table [z_j | h_j]: z_j is the canonical map column and h_j the
-// column of the parity check on the non-pivot (free) columns.  A query then
-// XORs the table entries of its set feature bits: the z part is T(phi) and
-// the h part is the reduction residual on the free columns, zero exactly when
-// phi lies in the span.
+// Encode (Sec. 2.3): T(phi) is the XOR of the canonical map columns over the
+// set bits of phi = [x | 1]; the support test checks phi against the
+// parity-check rows of the free (non-pivot) columns, which a prepare kernel
+// derives from the fitted basis.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -54,6 +55,7 @@ struct FitArgs {
     uint32_t* ctx_flags;
     int32_t* n_contra;
     int64_t* first_contra;
+    int32_t* plan;  // workspace: class list offsets, dynamic counters, context lists (k_fit_plan)
 };
 
 struct EncArgs {
@@ -103,10 +105,8 @@ __device__ __forceinline__ uint64_t top_mask(int n, int fw) {
 }
 
 // ---------------------------------------------------------------------------
-// context validation, shared by the fit kernels: a context is fitted by the
-// kernel of its width class; an invalid one gets rank 0 and a flag, written by
-// the register-basis kernel.  Each workgroup owns contexts g, g + G, g + 2G, ...
-// (G = grid size) and reads their descriptors 64 at a time, one per lane.
+// context descriptor: width, row segment and the checks of its offsets against
+// the buffer sizes (an invalid context is flagged and left at rank 0)
 // ---------------------------------------------------------------------------
 struct CtxDesc {
     int c, n;
@@ -152,25 +152,151 @@ __device__ __forceinline__ CtxDesc readlane_desc(const CtxDesc& v, int t) {
     return ds;
 }
 
-// width class of a valid context: 0 register basis (fw 1-3), 1 pivot-indexed LDS basis (fw 4-8), 2 large
-__device__ __forceinline__ int width_class(int n) {
-    const int fw = feat_words(n);
-    return fw <= 3 ? 0 : fw <= 8 ? 1 : 2;
-}
-
-// outputs of an invalid context (all lanes of one wavefront)
+// outputs of an invalid context (one thread)
 __device__ void write_bad_context(const FitArgs& a, const CtxDesc& ds) {
-    const int lane = threadIdx.x & 63;
-    if (lane == 0) {
-        a.rank[ds.c] = 0;
-        a.n_contra[ds.c] = 0;
-        a.first_contra[ds.c] = -1;
-        a.ctx_flags[ds.c] = ds.bad;
-    }
+    a.rank[ds.c] = 0;
+    a.n_contra[ds.c] = 0;
+    a.first_contra[ds.c] = -1;
+    a.ctx_flags[ds.c] = ds.bad;
     if (ds.bad == F2_CTX_BAD_SEGMENT) {
         const int64_t mo = a.map_off[ds.c];
-        for (int j = lane; j < 2 * (ds.n + 1); j += 64) a.maps[mo + j] = 0;
+        for (int j = 0; j < 2 * (ds.n + 1); ++j) a.maps[mo + j] = 0;
     }
+}
+
+// ---------------------------------------------------------------------------
+// fit plan.  Contexts are validated (an invalid one gets rank 0 and its flag
+// here), assigned to the kernel of their class, and each class list is sorted
+// by an estimate of the elimination work, largest first:
+//   class 0: fw <= 3, at most kLongRows rows  -> register basis, one wavefront
+//   class 1: fw 4-8, at most kLongRows rows   -> LDS basis, one wavefront
+//   class 2: fw <= 8, more than kLongRows rows -> LDS basis, kPivWaves wavefronts
+//   class 3: fw > 8                           -> large-context kernel
+// A class kernel with G workgroups deals its list out in stripes of G entries,
+// alternating direction from stripe to stripe, so that every workgroup gets a
+// similar share of the work and the longest contexts start first.  The sort is
+// a counting sort over (class, cost bucket) bins in three kernels (per-block
+// histograms, one scan, a scatter) with no device-wide atomics: on a chip of
+// eight dies those serialise far from the compute units.
+// Workspace (int32): [0, 5) list offsets per class, [16, 16 + C) the lists,
+// then C sort keys, kPlanBins bin bases and a kPlanBins histogram per plan block.
+// ---------------------------------------------------------------------------
+constexpr int kRegMaxFW = 3;
+constexpr int kPivMaxFW = 8;
+constexpr int kLongRows = 256;  // contexts with more rows take the multi-wavefront kernel
+enum { kClsReg = 0, kClsPiv = 1, kClsPivLong = 2, kClsLarge = 3, kNumCls = 4 };
+constexpr int kPlanHead = 16;
+constexpr int kBuckets = 256;
+constexpr int kPlanBins = kNumCls * kBuckets;
+constexpr int kPlanThreads = 1024;  // one context per thread; one bin per thread in the scan
+static_assert(kPlanBins == kPlanThreads, "the scan gives one bin to each thread");
+
+__device__ __forceinline__ int fit_class(const CtxDesc& ds) {
+    const int fw = feat_words(ds.n);
+    if (fw > kPivMaxFW) return kClsLarge;
+    if (ds.m > kLongRows) return kClsPivLong;
+    return fw <= kRegMaxFW ? kClsReg : kClsPiv;
+}
+
+// log-scale bucket (4 per octave) of rows x min(rows, d) x row words
+__device__ __forceinline__ int cost_bucket(const CtxDesc& ds) {
+    const uint64_t d = static_cast<uint64_t>(ds.n) + 1, W = static_cast<uint64_t>(feat_words(ds.n)) + F2_Y_WORDS;
+    const uint64_t m = ds.m < (1ll << 32) ? static_cast<uint64_t>(ds.m) : (1ull << 32);
+    const uint64_t cost = m * (m < d ? m : d) * W + 1;
+    const int e = 63 - __clzll(static_cast<long long>(cost));
+    const int frac = e >= 2 ? static_cast<int>((cost >> (e - 2)) & 3) : 0;
+    const int b = 4 * e + frac;
+    return b < kBuckets ? b : kBuckets - 1;
+}
+
+struct PlanView {
+    int32_t* cls_off;  // [kNumCls + 1]
+    int32_t* order;    // [C]
+    int32_t* key;      // [C]
+    int32_t* bin_base; // [kPlanBins]
+    int32_t* hist;     // [blocks][kPlanBins]
+};
+
+__device__ __forceinline__ PlanView plan_view(const FitArgs& a) {
+    PlanView v;
+    v.cls_off = a.plan;
+    v.order = a.plan + kPlanHead;
+    v.key = v.order + a.num_ctx;
+    v.bin_base = v.key + a.num_ctx;
+    v.hist = v.bin_base + kPlanBins;
+    return v;
+}
+
+// (1) per context: validate, class and bin; per block: histogram of the bins
+__global__ __launch_bounds__(kPlanThreads) void k_plan_count(FitArgs a) {
+    __shared__ int sBin[kPlanBins];
+    const PlanView P = plan_view(a);
+    const int tid = threadIdx.x;
+    sBin[tid] = 0;
+    __syncthreads();
+    const int64_t c = static_cast<int64_t>(blockIdx.x) * kPlanThreads + tid;
+    if (c < a.num_ctx) {
+        const CtxDesc ds = load_desc(a, c);
+        int k = -1;
+        if (ds.bad) {
+            write_bad_context(a, ds);
+        } else {
+            k = fit_class(ds) * kBuckets + (kBuckets - 1 - cost_bucket(ds));
+            atomicAdd(&sBin[k], 1);
+        }
+        P.key[c] = k;
+    }
+    __syncthreads();
+    P.hist[static_cast<int64_t>(blockIdx.x) * kPlanBins + tid] = sBin[tid];
+}
+
+// (2) one workgroup: per bin, exclusive prefix over the blocks; then the bin bases
+__global__ __launch_bounds__(kPlanThreads) void k_plan_scan(FitArgs a, int blocks) {
+    __shared__ int sWave[kPlanThreads / 64];
+    const PlanView P = plan_view(a);
+    const int tid = threadIdx.x, lane = tid & 63;
+    int total = 0;
+    for (int g = 0; g < blocks; ++g) {
+        int32_t* h = P.hist + static_cast<int64_t>(g) * kPlanBins + tid;
+        const int v = *h;
+        *h = total;
+        total += v;
+    }
+    int x = total;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(x, o);
+        if (lane >= o) x += t;
+    }
+    if (lane == 63) sWave[tid >> 6] = x;
+    __syncthreads();
+    int base = 0;
+    for (int w = 0; w < (tid >> 6); ++w) base += sWave[w];
+    const int excl = base + x - total;
+    P.bin_base[tid] = excl;
+    if (tid % kBuckets == 0) P.cls_off[tid / kBuckets] = excl;
+    if (tid == kPlanThreads - 1) P.cls_off[kNumCls] = excl + total;
+}
+
+// (3) scatter: list position = bin base + earlier blocks' count + rank within the block
+__global__ __launch_bounds__(kPlanThreads) void k_plan_scatter(FitArgs a) {
+    __shared__ int sBin[kPlanBins];
+    const PlanView P = plan_view(a);
+    const int tid = threadIdx.x;
+    sBin[tid] = P.bin_base[tid] + P.hist[static_cast<int64_t>(blockIdx.x) * kPlanBins + tid];
+    __syncthreads();
+    const int64_t c = static_cast<int64_t>(blockIdx.x) * kPlanThreads + tid;
+    if (c < a.num_ctx) {
+        const int k = P.key[c];
+        if (k >= 0) P.order[atomicAdd(&sBin[k], 1)] = static_cast<int32_t>(c);
+    }
+}
+
+// the i-th context of class cls dealt to this workgroup (snake order), or -1
+__device__ __forceinline__ int class_ctx(const FitArgs& a, int cls, int i) {
+    const int lo = a.plan[cls], cnt = a.plan[cls + 1] - lo;
+    const int G = static_cast<int>(gridDim.x), g = static_cast<int>(blockIdx.x);
+    const int64_t e = static_cast<int64_t>(i) * G + ((i & 1) ? G - 1 - g : g);
+    return e < cnt ? a.plan[kPlanHead + lo + static_cast<int>(e)] : -1;
 }
 
 // ---------------------------------------------------------------------------
@@ -209,8 +335,6 @@ __device__ __forceinline__ uint64_t xor_and(uint64_t f, uint32_t m, uint64_t d) 
     return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
-constexpr int kRegMaxFW = 3;
-constexpr int kLongRows = 256;  // contexts with more rows take the multi-wavefront kernel
 constexpr int kRecWords = 6;  // LDS record: fw feature words, 2 output words, pivot (<= 6 words)
 
 template <int FW>
@@ -431,23 +555,14 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
 __global__ __launch_bounds__(64) void k_fit_reg(FitArgs a) {
     __shared__ __align__(16) uint64_t sRec[64 * kRegMaxFW * kRecWords];
     __shared__ int16_t sPos[64 * kRegMaxFW];
-    const int lane = threadIdx.x;
-    for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
-        const CtxDesc mine = load_desc(a, blockIdx.x + (k0 + lane) * gridDim.x);
-        uint64_t todo = __ballot(mine.c >= 0 && (mine.bad || (width_class(mine.n) == 0 && mine.m <= kLongRows)));
-        while (todo) {
-            const int t = ffs64(todo);
-            todo &= todo - 1;
-            const CtxDesc ds = readlane_desc(mine, t);
-            if (ds.bad) {
-                write_bad_context(a, ds);
-                continue;
-            }
-            switch (feat_words(ds.n)) {
-                case 1: fit_ctx_reg<1>(a, ds, sRec, sPos); break;
-                case 2: fit_ctx_reg<2>(a, ds, sRec, sPos); break;
-                default: fit_ctx_reg<3>(a, ds, sRec, sPos); break;
-            }
+    for (int i = 0;; ++i) {
+        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsReg, i));
+        if (c < 0) break;
+        const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
+        switch (feat_words(ds.n)) {
+            case 1: fit_ctx_reg<1>(a, ds, sRec, sPos); break;
+            case 2: fit_ctx_reg<2>(a, ds, sRec, sPos); break;
+            default: fit_ctx_reg<3>(a, ds, sRec, sPos); break;
         }
     }
 }
@@ -463,7 +578,6 @@ __global__ __launch_bounds__(64) void k_fit_reg(FitArgs a) {
 // redone against the grown basis.  Once the basis stops growing every round
 // completes NW blocks.
 // ---------------------------------------------------------------------------
-constexpr int kPivMaxFW = 8;
 constexpr int kPivRec = kPivMaxFW + F2_Y_WORDS;  // record words
 constexpr int kPivCap = 64 * kPivMaxFW;          // d <= 512
 constexpr int kPivWaves = 8;
@@ -713,26 +827,17 @@ __device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
 template <int NW>
 __global__ __launch_bounds__(64 * NW) void k_fit_piv(FitArgs a) {
     __shared__ PivShared S;
-    const int tid = threadIdx.x, lane = tid & 63;
-    for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
-        // every wavefront reads the same 64 descriptors, so the ballot is uniform across the workgroup
-        const CtxDesc mine = load_desc(a, blockIdx.x + (k0 + lane) * gridDim.x);
-        const bool take = mine.c >= 0 && !mine.bad && width_class(mine.n) <= 1 &&
-                          (NW > 1 ? mine.m > kLongRows : (mine.m <= kLongRows && width_class(mine.n) == 1));
-        uint64_t todo = __ballot(take);
-        while (todo) {
-            const int t = ffs64(todo);
-            todo &= todo - 1;
-            const CtxDesc ds = readlane_desc(mine, t);
-            switch (feat_words(ds.n)) {
-                case 1: fit_ctx_piv<1, NW>(a, ds, S); break;
-                case 2: fit_ctx_piv<2, NW>(a, ds, S); break;
-                case 3: case 4: fit_ctx_piv<4, NW>(a, ds, S); break;
-                default: fit_ctx_piv<8, NW>(a, ds, S); break;
-            }
+    for (int i = 0;; ++i) {
+        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, NW > 1 ? kClsPivLong : kClsPiv, i));
+        if (c < 0) break;
+        const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
+        switch (feat_words(ds.n)) {
+            case 1: fit_ctx_piv<1, NW>(a, ds, S); break;
+            case 2: fit_ctx_piv<2, NW>(a, ds, S); break;
+            case 3: case 4: fit_ctx_piv<4, NW>(a, ds, S); break;
+            default: fit_ctx_piv<8, NW>(a, ds, S); break;
         }
     }
-    (void)tid;
 }
 
 // ---------------------------------------------------------------------------
@@ -756,7 +861,6 @@ __device__ __forceinline__ int slot_pivot(int t, int n) { return t < n ? n - 1 -
 
 constexpr int kLargeWaves = kLargeThreads / 64;
 constexpr int kRowsPerWave = kLargeRows / kLargeWaves;
-constexpr int kMaxD = F2_MAX_N_BITS + 1;
 
 // Stage the retained rows whose pivots are the set bits of pivot word pw into
 // dst[0 .. popc): wavefront v copies the rows of bits v, v+8, ... (lanes over
@@ -796,14 +900,11 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
     __shared__ long long sFirst, sFirstCons;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
-    for (int64_t k0 = 0; blockIdx.x + k0 * gridDim.x < a.num_ctx; k0 += 64) {
-      // every wavefront reads the same 64 descriptors, so the ballot is uniform across the workgroup
-      const CtxDesc mine = load_desc(a, blockIdx.x + (k0 + lane) * gridDim.x);
-      uint64_t todo = __ballot(mine.c >= 0 && !mine.bad && width_class(mine.n) == 2);
-      while (todo) {
-        const int tt = ffs64(todo);
-        todo &= todo - 1;
-        const CtxDesc ds = readlane_desc(mine, tt);
+    for (int i = 0;; ++i) {
+      const int cc = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsLarge, i));
+      if (cc < 0) break;
+      {
+        const CtxDesc ds = readlane_desc(load_desc(a, cc), 0);
         const int c = ds.c;
         const int n = ds.n;
         const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
@@ -1349,7 +1450,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs e) {
 
 inline size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
-// workgroups of a fit kernel: at most one per context, at most `cap`
+// workgroups of a fit class kernel: at most one per context, at most `cap`
 unsigned fit_grid(int num_ctx, int cap) { return static_cast<unsigned>(num_ctx < cap ? num_ctx : cap); }
 
 }  // namespace
@@ -1392,7 +1493,9 @@ int f2_fit_layout(const int32_t* n_bits_host, int32_t num_ctx, int64_t* basis_of
 
 size_t f2_fit_workspace_bytes(int32_t num_ctx) {
     if (num_ctx < 0) return 0;
-    return 256;  // reserved; the current kernels keep all scratch on chip
+    const size_t blocks = (static_cast<size_t>(num_ctx) + kPlanThreads - 1) / kPlanThreads;
+    return align256(sizeof(int32_t) *
+                    (kPlanHead + 2 * static_cast<size_t>(num_ctx) + kPlanBins * (1 + blocks)));
 }
 
 int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m,
@@ -1427,9 +1530,15 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     a.ctx_flags = m->ctx_flags;
     a.n_contra = m->n_contra;
     a.first_contra = m->first_contra_row;
-    hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid(C, 8192)), dim3(64), 0, s, a);
+    a.plan = static_cast<int32_t*>(workspace);
+    // each class kernel keeps about as many workgroups as fit on the chip at once
+    const int plan_blocks = static_cast<int>((static_cast<int64_t>(C) + kPlanThreads - 1) / kPlanThreads);
+    hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
+    hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kPlanThreads), 0, s, a, plan_blocks);
+    hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
+    hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid(C, 4096)), dim3(64), 0, s, a);
     hipLaunchKernelGGL(k_fit_piv<1>, dim3(fit_grid(C, 1024)), dim3(64), 0, s, a);
-    hipLaunchKernelGGL(k_fit_piv<kPivWaves>, dim3(fit_grid(C, 1024)), dim3(64 * kPivWaves), 0, s, a);
+    hipLaunchKernelGGL(k_fit_piv<kPivWaves>, dim3(fit_grid(C, 256)), dim3(64 * kPivWaves), 0, s, a);
     hipLaunchKernelGGL(k_fit_large, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
