@@ -85,6 +85,14 @@ enum {
  *                             column j = storage bit j; column p = z_p for every
  *                             pivot p and 0 for every other column (one linear
  *                             extension of T beyond the span, Sec. 2.3)
+ *   tables[basis_off[c] ...]  parity-check rows read by f2_encode_batch, present
+ *                             when t = n+1-rank <= rank: one row of fw words per
+ *                             free (non-pivot) column f, in ascending f: h_f = e_f
+ *                             plus e_p for every pivot p whose basis row holds
+ *                             bit f (t rows, within the basis capacity).  phi lies
+ *                             in the span exactly when every row has even overlap
+ *                             with it.  When t > rank the region is not written
+ *                             and encoding reduces phi by the basis rows instead.
  *   rank[c], ctx_flags[c], n_contra[c] (rows flagged contradictory),
  *   first_contra_row[c] (index within the context's segment, -1 if none).
  * For a contradictory context the stored map is defined by the rows kept in
@@ -103,6 +111,7 @@ typedef struct f2_model {
     uint64_t* basis;
     int32_t* pivots;
     uint64_t* maps;
+    uint64_t* tables;         /* basis_words words */
     int32_t* rank;            /* [num_ctx] */
     uint32_t* ctx_flags;      /* [num_ctx] */
     int32_t* n_contra;        /* [num_ctx] */
@@ -117,7 +126,8 @@ typedef struct f2_model {
 int f2_fit_layout(const int32_t* n_bits_host, int32_t num_ctx, int64_t* basis_off_host, int64_t* piv_off_host,
                   int64_t* map_off_host);
 
-/* Workspace bytes f2_fit_batch needs for num_ctx contexts (any widths). */
+/* Workspace bytes f2_fit_batch needs for num_ctx contexts (any widths): the
+ * per-batch plan that sorts contexts into kernel classes. */
 size_t f2_fit_workspace_bytes(int32_t num_ctx);
 
 /*
@@ -135,11 +145,8 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
                  void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * Workspace bytes f2_encode_batch needs for a fitted model and a batch size:
- * the per-context parity-check rows on the free columns (within the basis
- * capacity) and a zero column.  The batch size is part of the signature so the
- * encode path may use per-query scratch without an ABI change; the current one
- * needs none.
+ * Workspace bytes f2_encode_batch needs for a fitted model and a batch size
+ * (scratch for the batch; the model's tables are part of the fit outputs).
  */
 size_t f2_encode_workspace_bytes(const f2_model* model_host, int64_t num_queries);
 

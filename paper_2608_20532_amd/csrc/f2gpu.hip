@@ -51,6 +51,7 @@ struct FitArgs {
     uint64_t* basis;
     int32_t* pivots;
     uint64_t* maps;
+    uint64_t* tables;
     int32_t* rank;
     uint32_t* ctx_flags;
     int32_t* n_contra;
@@ -69,8 +70,7 @@ struct EncArgs {
     const uint32_t* ctx_flags;
     const int64_t* map_off;
     const uint64_t* maps;
-    uint64_t* tables;   // parity-check rows, context c at basis_off[c]
-    int64_t zero_word;  // tables[zero_word .. +2) is a zero column
+    const uint64_t* tables;  // parity-check rows, context c at basis_off[c]
     const int32_t* ctx_id;
     const uint64_t* x;
     int32_t stride;
@@ -299,6 +299,18 @@ __device__ __forceinline__ int class_ctx(const FitArgs& a, int cls, int i) {
     return e < cnt ? a.plan[kPlanHead + lo + static_cast<int>(e)] : -1;
 }
 
+// ---------------------------------------------------------------------------
+// parity-check rows, written by every fit kernel next to the canonical map:
+// for the i-th free (non-pivot) column f in ascending order, row i (fw words,
+// at the context's basis offset in the tables buffer) is h_f = e_f plus e_p for
+// every pivot p whose basis row holds bit f.  Since the basis is fully reduced,
+// the residual of reducing phi at column f is the parity of phi & h_f, so phi
+// lies in the span exactly when every row has even overlap with it.  Word w of
+// h_f is one ballot: lane b tests bit f of the basis row of pivot 64 w + b.
+// The rows exist only when t = d - rank <= rank; a context with more free
+// columns than basis rows is encoded by reducing phi with the basis itself.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool has_parity_rows(int d, int rank) { return d - rank <= rank; }
 // ---------------------------------------------------------------------------
 // register-basis fit (fw <= 3): one wavefront per context.  Lane s of register
 // set k holds retained row 64k + s (fw + 2 words and its pivot); the rows of
@@ -542,6 +554,31 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
         const int sl = sPos[j];
         a.maps[mo + 2 * j] = sl >= 0 ? sRec[sl * kRecWords + FW] : 0ull;
         a.maps[mo + 2 * j + 1] = sl >= 0 ? sRec[sl * kRecWords + FW + 1] : 0ull;
+    }
+    // parity-check rows of the free columns (sRec holds the final rows, sPos their slots)
+    uint64_t* H = a.tables + bo;
+    int slot[FW];
+#pragma unroll
+    for (int w = 0; w < FW; ++w) slot[w] = (64 * w + lane < d) ? sPos[64 * w + lane] : -1;
+    int i = 0;
+    const bool rows = has_parity_rows(d, rank);
+#pragma unroll
+    for (int w = 0; w < FW; ++w) {
+        uint64_t fr = rows ? ~pm[w] & (w == FW - 1 ? tmask : ~0ull) : 0ull;
+        while (fr) {
+            const int f = 64 * w + ffs64(fr);
+            fr &= fr - 1;
+            uint64_t hw_[FW];
+#pragma unroll
+            for (int v = 0; v < FW; ++v) {
+                const bool has = slot[v] >= 0 && ((sRec[(slot[v] < 0 ? 0 : slot[v]) * kRecWords + w] >> (f & 63)) & 1ull);
+                hw_[v] = __ballot(has) | (v == w ? (1ull << (f & 63)) : 0ull);
+            }
+#pragma unroll
+            for (int v = 0; v < FW; ++v)
+                if (lane == v) H[static_cast<int64_t>(i) * FW + v] = hw_[v];
+            ++i;
+        }
     }
     if (lane == 0) {
         a.rank[c] = rank;
@@ -787,7 +824,7 @@ __device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
     }
     __syncthreads();
 
-    // outputs: basis rows and pivots in descending priority, canonical map, scalars
+    // outputs: basis rows and pivots in descending priority, canonical map, encode table, scalars
     const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
     const int cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
@@ -813,6 +850,24 @@ __device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
         out[fw] = S.rec[j][FW];
         out[fw + 1] = S.rec[j][FW + 1];
         a.pivots[po + k] = j;
+    }
+    // parity-check rows of the free columns: wavefront v builds words v, v + NW, ...
+    uint64_t* H = a.tables + bo;
+    int i = 0;
+    const bool rows = has_parity_rows(d, rank);
+    for (int w = 0; w < fw && rows; ++w) {
+        uint64_t fr = ~S.pm[w] & (w == fw - 1 ? tmask : ~0ull);
+        while (fr) {
+            const int f = 64 * w + ffs64(fr);
+            fr &= fr - 1;
+            for (int v = wave; v < fw; v += NW) {
+                const int p = 64 * v + lane;
+                const bool has = ((S.pm[v] >> lane) & 1ull) && ((S.rec[p][w] >> (f & 63)) & 1ull);
+                const uint64_t hv = __ballot(has) | (v == w ? (1ull << (f & 63)) : 0ull);
+                if (lane == 0) H[static_cast<int64_t>(i) * fw + v] = hv;
+            }
+            ++i;
+        }
     }
     if (tid == 0) {
         a.rank[c] = rank;
@@ -1178,13 +1233,33 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
             if (tid == 0 && sFirst < 0 && sFirstCons != 0x7fffffffffffffffll) sFirst = sFirstCons;
         }
 
-        // outputs: canonical map from the slots, then compaction into descending priority
+        // outputs: canonical map and encode table from the slots, then compaction into descending priority
         const int64_t po = a.piv_off[c], mo = a.map_off[c];
         for (int j = tid; j < d; j += kLargeThreads) {
             const bool present = (sPmask[j >> 6] >> (j & 63)) & 1ull;
             const uint64_t* row = B + static_cast<int64_t>(prio_slot(j, n)) * W;
             a.maps[mo + 2 * j] = present ? row[fw] : 0ull;
             a.maps[mo + 2 * j + 1] = present ? row[fw + 1] : 0ull;
+        }
+        {  // parity-check rows of the free columns: wavefront v builds words v, v + 8, ...
+            uint64_t* H = a.tables + a.basis_off[c];
+            int i = 0;
+            const bool rows = has_parity_rows(d, rank);
+            for (int w = 0; w < fw && rows; ++w) {
+                uint64_t fr = ~sPmask[w] & (w == fw - 1 ? tmask : ~0ull);
+                while (fr) {
+                    const int f = 64 * w + ffs64(fr);
+                    fr &= fr - 1;
+                    for (int v = wave; v < fw; v += kLargeWaves) {
+                        const int p = 64 * v + lane;
+                        const bool piv = (sPmask[v] >> lane) & 1ull;
+                        const bool has = piv && ((B[static_cast<int64_t>(prio_slot(p, n)) * W + w] >> (f & 63)) & 1ull);
+                        const uint64_t hv = __ballot(has) | (v == w ? (1ull << (f & 63)) : 0ull);
+                        if (lane == 0) H[static_cast<int64_t>(i) * fw + v] = hv;
+                    }
+                    ++i;
+                }
+            }
         }
         __syncthreads();
         for (int t0 = 0; t0 < d; t0 += kLargeWaves) {
@@ -1230,92 +1305,11 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// encode.  T(phi) is the XOR of the canonical map columns M[j] over the set
-// feature bits j of phi = [x | 1] (M[p] = z_p on pivots, 0 elsewhere).  The
-// support test uses the parity check on the free (non-pivot) columns: for each
-// free column f, h_f = e_f + sum over pivots p of r_p[f] e_p; phi lies in the
-// span exactly when every h_f has even overlap with phi (the reduction residual
-// at f is that overlap).  k_enc_prepare writes the rows h_f of each context
-// (fw words each, in ascending f) into the workspace at the basis offsets.
+// encode (Sec. 2.3), one lane per query, queries in any order: the table
+// entries of the set bits of phi = [x | 1] are XORed (the constant column is
+// always set).  The z part is T(phi) = M phi; the h part is the reduction
+// residual on the free columns and must vanish for phi to lie in the span.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void k_enc_prepare(EncArgs e) {
-    __shared__ uint64_t sFree[64];
-    __shared__ int sFreeBefore[65];
-    __shared__ uint64_t sH[64][64];  // one parity-check row per lane
-    const int c = blockIdx.x, lane = threadIdx.x;
-    if (c >= e.num_ctx) return;
-    if (c == 0 && lane < 2) e.tables[e.zero_word + lane] = 0;  // a zero 16-byte column
-    if (e.ctx_flags[c] & kBadCtx) return;
-    const int n = e.n_bits[c];
-    const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
-    const int r = min(max(e.rank[c], 0), d);  // a model from f2_fit_batch always satisfies 0 <= rank <= d
-    const int t = d - r;
-    if (t == 0) return;
-    const uint64_t* B = e.basis + e.basis_off[c];
-    const int32_t* piv = e.pivots + e.piv_off[c];
-    uint64_t* H = e.tables + e.basis_off[c];
-    const uint64_t tmask = top_mask(n, fw);
-    for (int w = lane; w < fw; w += 64) sFree[w] = (w == fw - 1) ? tmask : ~0ull;
-    __syncthreads();
-    for (int k = lane; k < r; k += 64) {
-        const int p = min(max(piv[k], 0), n);
-        atomicAnd(reinterpret_cast<unsigned long long*>(&sFree[p >> 6]), ~(1ull << (p & 63)));
-    }
-    __syncthreads();
-    if (lane == 0) {
-        int acc = 0;
-        for (int w = 0; w < fw; ++w) {
-            sFreeBefore[w] = acc;
-            acc += __popcll(sFree[w]);
-        }
-        sFreeBefore[fw] = acc;
-    }
-    __syncthreads();
-    // free columns in ascending order, 64 per pass: row i of the pass is h of the
-    // (i0 + i)-th free column.  Lanes walk the retained rows: a set bit of r_k at a
-    // free column f of the pass puts the pivot of r_k into h_f.
-    for (int i0 = 0; i0 < t; i0 += 64) {
-        const int nrow = (t - i0) < 64 ? (t - i0) : 64;
-        for (int k = lane; k < nrow * fw; k += 64) sH[k / fw][k % fw] = 0;
-        __syncthreads();
-        // unit bit of each free column of the pass
-        for (int w = 0; w < fw; ++w) {
-            uint64_t v = sFree[w];
-            const int base = sFreeBefore[w];
-            if (base + __popcll(v) <= i0 || base >= i0 + nrow) continue;
-            if (lane < 64) {
-                // the lane-th set bit of this word, if it belongs to the pass
-                uint64_t u = v;
-                for (int skip = lane; skip > 0 && u; --skip) u &= u - 1;
-                const int idx = base + lane;
-                if (u && idx >= i0 && idx < i0 + nrow) {
-                    const int f = 64 * w + ffs64(u);
-                    atomicOr(reinterpret_cast<unsigned long long*>(&sH[idx - i0][f >> 6]), 1ull << (f & 63));
-                }
-            }
-        }
-        for (int k = lane; k < r; k += 64) {
-            const int p = min(max(piv[k], 0), n);
-            const uint64_t* row = B + static_cast<int64_t>(k) * W;
-            for (int w = 0; w < fw; ++w) {
-                const int base = sFreeBefore[w];
-                const uint64_t fr = sFree[w];
-                if (base + __popcll(fr) <= i0 || base >= i0 + nrow) continue;
-                uint64_t v = row[w] & fr;
-                while (v) {
-                    const int b = ffs64(v);
-                    v &= v - 1;
-                    const int idx = base + __popcll(fr & ((1ull << b) - 1));
-                    if (idx >= i0 && idx < i0 + nrow)
-                        atomicOr(reinterpret_cast<unsigned long long*>(&sH[idx - i0][p >> 6]), 1ull << (p & 63));
-                }
-            }
-        }
-        __syncthreads();
-        for (int k = lane; k < nrow * fw; k += 64) H[static_cast<int64_t>(i0) * fw + k] = sH[k / fw][k % fw];
-        __syncthreads();
-    }
-}
 
 // x words of a query, with bits past the stride read as zero
 template <int SMAX>
@@ -1323,12 +1317,12 @@ struct QueryX {
     uint64_t xr[SMAX > 0 ? SMAX : 1];
     const uint64_t* xq;
     int S;
-    __device__ __forceinline__ void load(const uint64_t* p, int stride, bool valid) {
+    __device__ __forceinline__ void load(const uint64_t* p, int stride) {
         xq = p;
         S = stride;
         if constexpr (SMAX > 0) {
 #pragma unroll
-            for (int k = 0; k < SMAX; ++k) xr[k] = (valid && k < S) ? p[k] : 0ull;
+            for (int k = 0; k < SMAX; ++k) xr[k] = k < S ? p[k] : 0ull;
         }
     }
     __device__ __forceinline__ uint64_t word(int w) const {
@@ -1355,13 +1349,51 @@ __device__ __forceinline__ bool outside_width(const QueryX<SMAX>& x, int n) {
     return outside;
 }
 
-// even overlap of phi = [x | 1] with every parity-check row of the context
+struct alignas(16) Word2 {
+    uint64_t x, y;
+};
+
+// T(phi): XOR of the map columns of the set bits, four gathers in flight
 template <int SMAX>
-__device__ __forceinline__ bool parity_ok(const EncArgs& e, int c, int n, const QueryX<SMAX>& x) {
-    const int fw = feat_words(n), d = n + 1;
-    const int t = d - min(max(e.rank[c], 0), d);
-    const uint64_t* H = e.tables + e.basis_off[c];
-    const int cw = n >> 6;
+__device__ __forceinline__ void map_gather(const uint64_t* M, int n, const QueryX<SMAX>& x, uint64_t& z0,
+                                           uint64_t& z1) {
+    const Word2 zc = *reinterpret_cast<const Word2*>(M + 2 * n);  // constant column: always set
+    z0 = zc.x;
+    z1 = zc.y;
+    const int fw = feat_words(n);
+    const int xw = x.S < fw ? x.S : fw;
+    for (int w = 0; w < xw; ++w) {
+        const uint64_t v = x.word(w);
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            uint32_t u = half ? static_cast<uint32_t>(v >> 32) : static_cast<uint32_t>(v);
+            const uint64_t* Mh = M + 2 * (64 * w + 32 * half);
+            while (u) {  // a missing gather re-reads the first column and is masked off
+                int jj[4];
+                uint64_t mk[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    mk[k] = u ? ~0ull : 0ull;
+                    jj[k] = u ? __builtin_ctz(u) : jj[0];
+                    u &= u - 1;
+                }
+                Word2 a[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) a[k] = *reinterpret_cast<const Word2*>(Mh + 2 * jj[k]);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    z0 ^= a[k].x & mk[k];
+                    z1 ^= a[k].y & mk[k];
+                }
+            }
+        }
+    }
+}
+
+// support test: even overlap of phi = [x | 1] with every parity-check row
+template <int SMAX>
+__device__ __forceinline__ bool parity_ok(const uint64_t* H, int t, int n, const QueryX<SMAX>& x) {
+    const int fw = feat_words(n), cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
     for (int f = 0; f < t; ++f) {
         const uint64_t* h = H + static_cast<int64_t>(f) * fw;
@@ -1376,46 +1408,76 @@ __device__ __forceinline__ bool parity_ok(const EncArgs& e, int c, int n, const 
     return true;
 }
 
-// per-lane encode by gathering the map columns of the set bits (lanes may hold different contexts)
+// low-rank contexts: reduce phi by the basis rows (descending priority); the
+// rows whose pivot bit phi holds sum to [phi | T(phi)] exactly when phi is in the span
 template <int SMAX>
-__device__ __forceinline__ bool encode_gather(const EncArgs& e, int c, const QueryX<SMAX>& x, uint64_t& z0,
-                                              uint64_t& z1) {
-    const int n = e.n_bits[c];
-    const int fw = feat_words(n);
-    if (outside_width(x, n)) return false;
-    const uint64_t* M = e.maps + e.map_off[c];
-    const uint64_t* Z = e.tables + e.zero_word;
-    z0 = M[2 * n];  // constant column: always set
-    z1 = M[2 * n + 1];
-    const int xw = x.S < fw ? x.S : fw;
-    for (int w = 0; w < xw; ++w) {
-        const uint64_t v = x.word(w);
+__device__ __forceinline__ bool basis_scan(const uint64_t* B, const int32_t* piv, int rank, int n,
+                                           const QueryX<SMAX>& x, uint64_t& z0, uint64_t& z1) {
+    const int fw = feat_words(n), W = fw + F2_Y_WORDS, cw = n >> 6;
+    const uint64_t cbit = 1ull << (n & 63);
+    uint64_t diff = 0;  // features: phi XOR the selected rows, word by word
+    z0 = z1 = 0;
+    if (fw <= 4) {
+        uint64_t acc[4] = {0, 0, 0, 0};
+        for (int k = 0; k < rank; ++k) {
+            const int p = piv[k];
+            uint64_t qw = x.word(p >> 6);
+            if ((p >> 6) == cw) qw |= cbit;
+            const uint64_t mk = 0ull - ((qw >> (p & 63)) & 1ull);
+            const uint64_t* row = B + static_cast<int64_t>(k) * W;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            uint32_t u = h ? static_cast<uint32_t>(v >> 32) : static_cast<uint32_t>(v);
-            const uint64_t* Mh = M + 2 * (64 * w + 32 * h);
-            while (u) {  // four gathers in flight; missing ones read a zero column
-                const uint64_t* p0 = Mh + 2 * __builtin_ctz(u);
-                u &= u - 1;
-                const uint64_t* p1 = u ? Mh + 2 * __builtin_ctz(u) : Z;
-                u &= u - 1;
-                const uint64_t* p2 = u ? Mh + 2 * __builtin_ctz(u) : Z;
-                u &= u - 1;
-                const uint64_t* p3 = u ? Mh + 2 * __builtin_ctz(u) : Z;
-                u &= u - 1;
-                const ulonglong2 a0 = *reinterpret_cast<const ulonglong2*>(p0);
-                const ulonglong2 a1 = *reinterpret_cast<const ulonglong2*>(p1);
-                const ulonglong2 a2 = *reinterpret_cast<const ulonglong2*>(p2);
-                const ulonglong2 a3 = *reinterpret_cast<const ulonglong2*>(p3);
-                z0 ^= a0.x ^ a1.x ^ a2.x ^ a3.x;
-                z1 ^= a0.y ^ a1.y ^ a2.y ^ a3.y;
+            for (int w = 0; w < 4; ++w)
+                if (w < fw) acc[w] ^= row[w] & mk;
+            z0 ^= row[fw] & mk;
+            z1 ^= row[fw + 1] & mk;
+        }
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            if (w >= fw) break;
+            uint64_t qw = x.word(w);
+            if (w == cw) qw |= cbit;
+            diff |= acc[w] ^ qw;
+        }
+    } else {
+        for (int w = 0; w < fw; ++w) {  // one feature word at a time
+            uint64_t acc = 0;
+            for (int k = 0; k < rank; ++k) {
+                const int p = piv[k];
+                uint64_t qw = x.word(p >> 6);
+                if ((p >> 6) == cw) qw |= cbit;
+                if ((qw >> (p & 63)) & 1ull) {
+                    const uint64_t* row = B + static_cast<int64_t>(k) * W;
+                    acc ^= row[w];
+                    if (w == 0) {
+                        z0 ^= row[fw];
+                        z1 ^= row[fw + 1];
+                    }
+                }
             }
+            uint64_t qw = x.word(w);
+            if (w == cw) qw |= cbit;
+            diff |= acc ^ qw;
         }
     }
-    return parity_ok(e, c, n, x);
+    return diff == 0;
 }
 
-// one lane per query, queries in arbitrary order
+template <int SMAX>
+__device__ __forceinline__ bool encode_query(const EncArgs& e, int c, const uint64_t* xq, uint64_t& z0,
+                                             uint64_t& z1) {
+    QueryX<SMAX> x;
+    x.load(xq, e.stride);
+    const int n = e.n_bits[c];
+    if (outside_width(x, n)) return false;
+    const int d = n + 1;
+    const int r0 = e.rank[c];
+    const int r = r0 < 0 ? 0 : (r0 > d ? d : r0);  // 0 <= rank <= d for a fitted context
+    if (!has_parity_rows(d, r))
+        return basis_scan(e.basis + e.basis_off[c], e.pivots + e.piv_off[c], r, n, x, z0, z1);
+    map_gather(e.maps + e.map_off[c], n, x, z0, z1);
+    return parity_ok(e.tables + e.basis_off[c], d - r, n, x);
+}
+
 __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs e) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
     if (q >= e.nq) return;
@@ -1426,25 +1488,17 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs e) {
         fl = F2_Q_BAD_CTX;
     } else {
         if (e.ctx_flags[c] & F2_CTX_CONTRADICTION) fl = F2_Q_CTX_CONTRADICTORY;
-        bool in;
-        if (e.stride <= 4) {
-            QueryX<4> x;
-            x.load(e.x + q * e.stride, e.stride, true);
-            in = encode_gather(e, c, x, z0, z1);
-        } else {
-            QueryX<0> x;
-            x.load(e.x + q * e.stride, e.stride, true);
-            in = encode_gather(e, c, x, z0, z1);
-        }
+        const uint64_t* xq = e.x + q * e.stride;
+        const bool in = e.stride <= 4 ? encode_query<4>(e, c, xq, z0, z1) : encode_query<0>(e, c, xq, z0, z1);
         if (!in) {
             fl |= F2_Q_OUT_OF_SPAN;
             z0 = z1 = 0;
         }
     }
-    ulonglong2 out;
+    Word2 out;
     out.x = z0;
     out.y = z1;
-    *reinterpret_cast<ulonglong2*>(e.words + 2 * q) = out;
+    *reinterpret_cast<Word2*>(e.words + 2 * q) = out;
     e.qflags[q] = fl;
 }
 
@@ -1504,7 +1558,7 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     const int32_t C = m->num_ctx;
     if (C == 0) return F2_OK;
     if (!row_off || !m->n_bits || !m->basis_off || !m->piv_off || !m->map_off || !m->basis || !m->pivots ||
-        !m->maps || !m->rank || !m->ctx_flags || !m->n_contra || !m->first_contra_row || (rows_words > 0 && !rows) ||
+        !m->maps || !m->tables || !m->rank || !m->ctx_flags || !m->n_contra || !m->first_contra_row || (rows_words > 0 && !rows) ||
         m->basis_words < 0 || m->piv_entries < 0 || m->map_words < 0)
         return F2_EINVAL;
     if (!workspace || workspace_bytes < f2_fit_workspace_bytes(C) ||
@@ -1526,6 +1580,7 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     a.basis = m->basis;
     a.pivots = m->pivots;
     a.maps = m->maps;
+    a.tables = m->tables;
     a.rank = m->rank;
     a.ctx_flags = m->ctx_flags;
     a.n_contra = m->n_contra;
@@ -1544,8 +1599,8 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
 }
 
 size_t f2_encode_workspace_bytes(const f2_model* m, int64_t num_queries) {
-    if (!m || m->basis_words < 0 || m->num_ctx < 0 || num_queries < 0) return 0;
-    return align256(sizeof(uint64_t) * static_cast<size_t>(m->basis_words)) + 256;
+    if (!m || m->num_ctx < 0 || num_queries < 0) return 0;
+    return 256;  // reserved
 }
 
 int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x, int32_t x_stride_words,
@@ -1555,7 +1610,7 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     if (num_queries == 0) return F2_OK;
     if (!ctx_id || !x || !words_out || !qflags_out) return F2_EINVAL;
     if (m->num_ctx > 0 && (!m->n_bits || !m->basis_off || !m->piv_off || !m->map_off || !m->basis || !m->pivots ||
-                           !m->maps || !m->rank || !m->ctx_flags))
+                           !m->maps || !m->tables || !m->rank || !m->ctx_flags))
         return F2_EINVAL;
     if (!workspace || workspace_bytes < f2_encode_workspace_bytes(m, num_queries) ||
         (reinterpret_cast<uintptr_t>(workspace) & 255u))
@@ -1572,8 +1627,7 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     e.ctx_flags = m->ctx_flags;
     e.map_off = m->map_off;
     e.maps = m->maps;
-    e.tables = static_cast<uint64_t*>(workspace);
-    e.zero_word = static_cast<int64_t>(align256(sizeof(uint64_t) * static_cast<size_t>(m->basis_words)) / 8);
+    e.tables = m->tables;
     e.ctx_id = ctx_id;
     e.x = x;
     e.stride = x_stride_words;
@@ -1582,7 +1636,6 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     e.qflags = qflags_out;
     const int64_t blocks = (num_queries + kEncThreads - 1) / kEncThreads;
     if (blocks > 0x7fffffff) return F2_EINVAL;
-    hipLaunchKernelGGL(k_enc_prepare, dim3(m->num_ctx > 0 ? m->num_ctx : 1), dim3(64), 0, s, e);
     hipLaunchKernelGGL(k_encode, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }

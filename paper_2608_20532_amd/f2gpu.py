@@ -41,6 +41,7 @@ class f2_model(ctypes.Structure):
         ("basis", ctypes.c_void_p),
         ("pivots", ctypes.c_void_p),
         ("maps", ctypes.c_void_p),
+        ("tables", ctypes.c_void_p),
         ("rank", ctypes.c_void_p),
         ("ctx_flags", ctypes.c_void_p),
         ("n_contra", ctypes.c_void_p),
@@ -129,6 +130,7 @@ class Model:
         self.basis = torch.zeros(max(int(bo[-1]), 1), dtype=torch.int64, device=dev)
         self.pivots = torch.zeros(max(int(po[-1]), 1), dtype=torch.int32, device=dev)
         self.maps = torch.zeros(max(int(mo[-1]), 1), dtype=torch.int64, device=dev)
+        self.tables = torch.zeros(max(int(bo[-1]), 1), dtype=torch.int64, device=dev)
         self.rank = torch.zeros(C, dtype=torch.int32, device=dev)
         self.ctx_flags = torch.zeros(C, dtype=torch.int32, device=dev)
         self.n_contra = torch.zeros(C, dtype=torch.int32, device=dev)
@@ -140,7 +142,8 @@ class Model:
             self._struct = f2_model(
                 self.num_ctx, _ptr(self.n_bits), _ptr(self.basis_off), _ptr(self.piv_off), _ptr(self.map_off),
                 int(self.basis_off_host[-1]), int(self.piv_off_host[-1]), int(self.map_off_host[-1]),
-                _ptr(self.basis), _ptr(self.pivots), _ptr(self.maps), _ptr(self.rank), _ptr(self.ctx_flags),
+                _ptr(self.basis), _ptr(self.pivots), _ptr(self.maps), _ptr(self.tables), _ptr(self.rank),
+                _ptr(self.ctx_flags),
                 _ptr(self.n_contra), _ptr(self.first_contra_row))
         return self._struct
 

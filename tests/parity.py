@@ -29,6 +29,7 @@ def gpu_fit(f2, rows, row_off, n_bits):
 def model_to_host(model):
     return dict(
         basis=host(model.basis, np.uint64), pivots=host(model.pivots, np.int32), maps=host(model.maps, np.uint64),
+        tables=host(model.tables, np.uint64),
         rank=host(model.rank, np.int32)[:model.num_ctx], flags=host(model.ctx_flags, np.uint32)[:model.num_ctx],
         n_contra=host(model.n_contra, np.int32)[:model.num_ctx],
         first=host(model.first_contra_row, np.int64)[:model.num_ctx])
@@ -63,7 +64,38 @@ def compare_fit(model, ref: "oracle.FitResult", ctx=None):
     bad = np.nonzero(g["basis"][:len(bmask)][bmask] != ref.basis[bmask])[0]
     assert len(bad) == 0, f"basis mismatch at {len(bad)} words"
     assert np.array_equal(g["maps"][:len(mmask)][mmask], ref.maps[mmask]), "maps"
+    check = np.nonzero(ok_ctx & ((ref.flags[:C] & oracle.CTX_BAD_SEGMENT) == 0))[0]
+    if ctx is not None:
+        check = np.intersect1d(check, np.asarray(ctx))
+    for c in check:
+        d = int(ref.n_bits[c]) + 1
+        if d - int(ref.rank[c]) > int(ref.rank[c]):
+            continue  # no parity rows: encoding reduces by the basis
+        exp = expected_table(ref, int(c))
+        got = g["tables"][ref.basis_off[c]:ref.basis_off[c] + exp.size]
+        assert np.array_equal(got, exp), f"parity-check rows of context {c}"
     return C
+
+
+def expected_table(ref: "oracle.FitResult", c: int) -> np.ndarray:
+    """Parity-check rows of context c derived from the oracle's basis: for each free
+    (non-pivot) column f in ascending order, fw words holding bit f and the pivot of
+    every basis row that has bit f set (the layout documented for f2_model.tables)."""
+    piv, B, M = ref.context(c)
+    n = int(ref.n_bits[c])
+    d = n + 1
+    fw = (n + 64) // 64
+    is_piv = np.zeros(d, bool)
+    is_piv[piv] = True
+    free = np.nonzero(~is_piv)[0]
+    hb = np.zeros((len(free), 64 * fw), bool)
+    hb[np.arange(len(free)), free] = True
+    if len(piv) and len(free):
+        feat = np.unpackbits(np.ascontiguousarray(B[:, :fw]).view(np.uint8), axis=1, bitorder="little")
+        sel = feat[:, free].astype(bool)          # [rank, t]: basis row k holds free column f
+        for k, p in enumerate(piv):
+            hb[sel[k], p] = True
+    return np.packbits(hb, axis=1, bitorder="little").view(np.uint64).ravel()
 
 
 def compare_encode(words_dev, qf_dev, ref_words, ref_qf, sample=None):

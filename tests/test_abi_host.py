@@ -52,12 +52,16 @@ def test_status_strings_and_workspace_sizes():
     for st in (0, -1, -2, -3, -4):
         assert f2gpu.f2_status_string(st) != "unknown status"
     assert f2gpu.f2_status_string(7) == "unknown status"
-    assert f2gpu.f2_fit_workspace_bytes(10) >= 1 and f2gpu.f2_fit_workspace_bytes(-1) == 0
+    assert f2gpu.f2_fit_workspace_bytes(-1) == 0
+    # the fit plan holds a context list and a sort key per context
+    assert f2gpu.f2_fit_workspace_bytes(100_000) >= 8 * 100_000 > f2gpu.f2_fit_workspace_bytes(10) > 0
+    assert f2gpu.f2_fit_workspace_bytes(10) % 256 == 0
     m = f2gpu.f2_model()
     m.num_ctx, m.basis_words = 10, 1000
     small = f2gpu.lib.f2_encode_workspace_bytes(ctypes.byref(m), 1000)
     big = f2gpu.lib.f2_encode_workspace_bytes(ctypes.byref(m), 1 << 20)
-    assert small >= 8000 and big >= small   # parity rows live within the basis capacity
+    assert 0 < small <= big and small % 256 == 0 and big % 256 == 0
+    assert f2gpu.lib.f2_encode_workspace_bytes(ctypes.byref(m), -1) == 0
 
 
 def test_calls_with_bad_host_arguments_enqueue_nothing():
