@@ -1391,21 +1391,33 @@ __device__ __forceinline__ void map_gather(const uint64_t* M, int n, const Query
 }
 
 // support test: even overlap of phi = [x | 1] with every parity-check row
+// (all rows are read, several at a time: no early exit to serialise the loads)
 template <int SMAX>
 __device__ __forceinline__ bool parity_ok(const uint64_t* H, int t, int n, const QueryX<SMAX>& x) {
     const int fw = feat_words(n), cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
-    for (int f = 0; f < t; ++f) {
-        const uint64_t* h = H + static_cast<int64_t>(f) * fw;
-        uint64_t acc = 0;
-        for (int w = 0; w < fw; ++w) {
-            uint64_t qw = x.word(w);
-            if (w == cw) qw |= cbit;
-            acc ^= h[w] & qw;
+    int odd = 0;  // bit 0 of an OR of popcounts is the OR of their parities
+    if (fw == 1) {
+        const uint64_t q = x.word(0) | cbit;
+        int f = 0;
+        for (; f + 4 <= t; f += 4) {
+            const uint64_t h0 = H[f], h1 = H[f + 1], h2 = H[f + 2], h3 = H[f + 3];
+            odd |= __popcll(h0 & q) | __popcll(h1 & q) | __popcll(h2 & q) | __popcll(h3 & q);
         }
-        if (__popcll(acc) & 1) return false;
+        for (; f < t; ++f) odd |= __popcll(H[f] & q);
+    } else {
+        for (int f = 0; f < t; ++f) {
+            const uint64_t* h = H + static_cast<int64_t>(f) * fw;
+            uint64_t acc = 0;
+            for (int w = 0; w < fw; ++w) {
+                uint64_t qw = x.word(w);
+                if (w == cw) qw |= cbit;
+                acc ^= h[w] & qw;
+            }
+            odd |= __popcll(acc);
+        }
     }
-    return true;
+    return (odd & 1) == 0;
 }
 
 // low-rank contexts: reduce phi by the basis rows (descending priority); the
@@ -1419,17 +1431,39 @@ __device__ __forceinline__ bool basis_scan(const uint64_t* B, const int32_t* piv
     z0 = z1 = 0;
     if (fw <= 4) {
         uint64_t acc[4] = {0, 0, 0, 0};
-        for (int k = 0; k < rank; ++k) {
-            const int p = piv[k];
+        auto add_row = [&](int p, const uint64_t (&rv)[6]) {
             uint64_t qw = x.word(p >> 6);
             if ((p >> 6) == cw) qw |= cbit;
             const uint64_t mk = 0ull - ((qw >> (p & 63)) & 1ull);
-            const uint64_t* row = B + static_cast<int64_t>(k) * W;
 #pragma unroll
-            for (int w = 0; w < 4; ++w)
-                if (w < fw) acc[w] ^= row[w] & mk;
-            z0 ^= row[fw] & mk;
-            z1 ^= row[fw + 1] & mk;
+            for (int w = 0; w < 4; ++w) acc[w] ^= rv[w] & mk;
+            z0 ^= rv[4] & mk;
+            z1 ^= rv[5] & mk;
+        };
+        int k = 0;
+        for (; k + 4 <= rank; k += 4) {  // four rows in flight
+            int p[4];
+            uint64_t rv[4][6];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                p[u] = piv[k + u];
+                const uint64_t* row = B + static_cast<int64_t>(k + u) * W;
+#pragma unroll
+                for (int w = 0; w < 4; ++w) rv[u][w] = w < fw ? row[w] : 0ull;
+                rv[u][4] = row[fw];
+                rv[u][5] = row[fw + 1];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) add_row(p[u], rv[u]);
+        }
+        for (; k < rank; ++k) {
+            const uint64_t* row = B + static_cast<int64_t>(k) * W;
+            uint64_t rv[6];
+#pragma unroll
+            for (int w = 0; w < 4; ++w) rv[w] = w < fw ? row[w] : 0ull;
+            rv[4] = row[fw];
+            rv[5] = row[fw + 1];
+            add_row(piv[k], rv);
         }
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
@@ -1478,34 +1512,238 @@ __device__ __forceinline__ bool encode_query(const EncArgs& e, int c, const uint
     return parity_ok(e.tables + e.basis_off[c], d - r, n, x);
 }
 
+// flags and word of one query of context id c
+__device__ __forceinline__ uint8_t encode_one(const EncArgs& e, int c, int64_t q, uint64_t& z0, uint64_t& z1) {
+    z0 = z1 = 0;
+    if (c < 0 || c >= e.num_ctx || (e.ctx_flags[c] & kBadCtx)) return F2_Q_BAD_CTX;
+    uint8_t fl = (e.ctx_flags[c] & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0;
+    const uint64_t* xq = e.x + q * e.stride;
+    const bool in = e.stride <= 4 ? encode_query<4>(e, c, xq, z0, z1) : encode_query<0>(e, c, xq, z0, z1);
+    if (!in) {
+        fl |= F2_Q_OUT_OF_SPAN;
+        z0 = z1 = 0;
+    }
+    return fl;
+}
+
 __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs e) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
     if (q >= e.nq) return;
-    const int c = e.ctx_id[q];
-    uint64_t z0 = 0, z1 = 0;
-    uint8_t fl = 0;
-    if (c < 0 || c >= e.num_ctx || (e.ctx_flags[c] & kBadCtx)) {
-        fl = F2_Q_BAD_CTX;
-    } else {
-        if (e.ctx_flags[c] & F2_CTX_CONTRADICTION) fl = F2_Q_CTX_CONTRADICTORY;
-        const uint64_t* xq = e.x + q * e.stride;
-        const bool in = e.stride <= 4 ? encode_query<4>(e, c, xq, z0, z1) : encode_query<0>(e, c, xq, z0, z1);
-        if (!in) {
-            fl |= F2_Q_OUT_OF_SPAN;
-            z0 = z1 = 0;
-        }
-    }
     Word2 out;
-    out.x = z0;
-    out.y = z1;
+    const uint8_t fl = encode_one(e, e.ctx_id[q], q, out.x, out.y);
     *reinterpret_cast<Word2*>(e.words + 2 * q) = out;
     e.qflags[q] = fl;
+}
+
+// ---------------------------------------------------------------------------
+// context-grouped encode for large batches.  In arbitrary order the lanes of a
+// wavefront gather from as many maps as they hold contexts, one cache line per
+// lane.  A counting sort by bin (2^k consecutive contexts per bin, at most
+// kSortMaxBins bins, one more bin for out-of-range ids) first groups the
+// queries; the encode then runs over the sorted order, where the lanes of a
+// wavefront share a few contexts and their gathers hit the same lines; a last
+// pass returns the results to query order (up to kDirectMaxQueries queries the
+// results are written straight to their queries instead: scattered writes of a
+// batch that size merge in the last-level cache, larger ones pay for the extra
+// pass with coalesced writes).  The sort uses per-block LDS
+// histograms and scans (no device-wide atomics):
+//   count (per block)  ->  column scan (per bin, over blocks)  ->  bin scan
+//   ->  scatter (query -> sorted position)  ->  sorted encode  ->  unsort
+// ---------------------------------------------------------------------------
+constexpr int kSortThreads = 1024;
+constexpr int kSortMaxBins = 8192;
+constexpr int64_t kDirectMaxQueries = 1 << 22;
+
+struct SortArgs {
+    int32_t direct;   // 1: the sorted encode writes each result at its query; 0: through res and the unsort
+    int32_t nb;       // bins, the last one for out-of-range context ids
+    int32_t bin_shift;  // 2^bin_shift contexts per bin
+    int32_t blocks;   // count / scatter blocks
+    int64_t qc;       // queries per count / scatter block
+    int32_t* hist;    // [blocks][nb], then exclusive offsets within each bin
+    int32_t* total;   // [nb]
+    int32_t* base;    // [nb] first sorted position of each bin
+    int2* perm;       // [nq] sorted position -> (query, context id)
+    int32_t* pos;     // [nq] query -> sorted position
+    Word2* res;       // [2 nq] sorted position -> word, flags
+};
+
+__device__ __forceinline__ int query_bin(const EncArgs& e, const SortArgs& s, int c) {
+    return (c < 0 || c >= e.num_ctx) ? s.nb - 1 : (c >> s.bin_shift);
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_enc_count(EncArgs e, SortArgs s) {
+    __shared__ int sBin[kSortMaxBins + 1];
+    const int tid = threadIdx.x;
+    for (int b = tid; b < s.nb; b += kSortThreads) sBin[b] = 0;
+    __syncthreads();
+    const int64_t q0 = static_cast<int64_t>(blockIdx.x) * s.qc;
+    const int64_t q1 = q0 + s.qc < e.nq ? q0 + s.qc : e.nq;
+    int64_t q = q0 + tid;
+    for (; q + 3 * kSortThreads < q1; q += 4 * kSortThreads) {
+        int c[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) c[u] = e.ctx_id[q + u * kSortThreads];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) atomicAdd(&sBin[query_bin(e, s, c[u])], 1);
+    }
+    for (; q < q1; q += kSortThreads) atomicAdd(&sBin[query_bin(e, s, e.ctx_id[q])], 1);
+    __syncthreads();
+    int32_t* h = s.hist + static_cast<int64_t>(blockIdx.x) * s.nb;
+    for (int b = tid; b < s.nb; b += kSortThreads) h[b] = sBin[b];
+}
+
+// one thread per bin: exclusive prefix over the blocks, in place; the bin's total
+__global__ __launch_bounds__(256) void k_enc_colscan(SortArgs s) {
+    const int b = blockIdx.x * 256 + threadIdx.x;
+    if (b >= s.nb) return;
+    int run = 0;
+    int g = 0;
+    for (; g + 8 <= s.blocks; g += 8) {  // eight loads in flight
+        int v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = s.hist[static_cast<int64_t>(g + k) * s.nb + b];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            s.hist[static_cast<int64_t>(g + k) * s.nb + b] = run;
+            run += v[k];
+        }
+    }
+    for (; g < s.blocks; ++g) {
+        int32_t* h = s.hist + static_cast<int64_t>(g) * s.nb + b;
+        const int v = *h;
+        *h = run;
+        run += v;
+    }
+    s.total[b] = run;
+}
+
+// one workgroup: exclusive scan of the bin totals
+__global__ __launch_bounds__(kSortThreads) void k_enc_binscan(SortArgs s) {
+    __shared__ int sWave[kSortThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int per = (s.nb + kSortThreads - 1) / kSortThreads;
+    const int b0 = tid * per;
+    int sum = 0;
+    for (int k = 0; k < per; ++k)
+        if (b0 + k < s.nb) sum += s.total[b0 + k];
+    int x = sum;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(x, o);
+        if (lane >= o) x += t;
+    }
+    if (lane == 63) sWave[tid >> 6] = x;
+    __syncthreads();
+    int run = x - sum;
+    for (int w = 0; w < (tid >> 6); ++w) run += sWave[w];
+    for (int k = 0; k < per; ++k)
+        if (b0 + k < s.nb) {
+            s.base[b0 + k] = run;
+            run += s.total[b0 + k];
+        }
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_enc_scatter(EncArgs e, SortArgs s) {
+    __shared__ int sBin[kSortMaxBins + 1];
+    const int tid = threadIdx.x;
+    const int32_t* h = s.hist + static_cast<int64_t>(blockIdx.x) * s.nb;
+    for (int b = tid; b < s.nb; b += kSortThreads) sBin[b] = s.base[b] + h[b];
+    __syncthreads();
+    const int64_t q0 = static_cast<int64_t>(blockIdx.x) * s.qc;
+    const int64_t q1 = q0 + s.qc < e.nq ? q0 + s.qc : e.nq;
+    auto place = [&](int64_t q, int c, int p) {
+        s.perm[p] = make_int2(static_cast<int>(q), c);
+        if (!s.direct) s.pos[q] = p;
+    };
+    int64_t q = q0 + tid;
+    for (; q + 3 * kSortThreads < q1; q += 4 * kSortThreads) {
+        int c[4], p[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) c[u] = e.ctx_id[q + u * kSortThreads];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) p[u] = atomicAdd(&sBin[query_bin(e, s, c[u])], 1);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) place(q + u * kSortThreads, c[u], p[u]);
+    }
+    for (; q < q1; q += kSortThreads) {
+        const int c = e.ctx_id[q];
+        place(q, c, atomicAdd(&sBin[query_bin(e, s, c)], 1));
+    }
+}
+
+__global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortArgs s) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
+    if (i >= e.nq) return;
+    const int2 qc = s.perm[i];
+    Word2 out, fl;
+    fl.x = encode_one(e, qc.y, qc.x, out.x, out.y);
+    fl.y = 0;
+    if (s.direct) {
+        *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
+        e.qflags[qc.x] = static_cast<uint8_t>(fl.x);
+    } else {
+        s.res[2 * i] = out;
+        s.res[2 * i + 1] = fl;
+    }
+}
+
+__global__ __launch_bounds__(kEncThreads) void k_enc_unsort(EncArgs e, SortArgs s) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
+    if (q >= e.nq) return;
+    const int64_t i = s.pos[q];
+    *reinterpret_cast<Word2*>(e.words + 2 * q) = s.res[2 * i];
+    e.qflags[q] = static_cast<uint8_t>(s.res[2 * i + 1].x);
 }
 
 inline size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
 // workgroups of a fit class kernel: at most one per context, at most `cap`
 unsigned fit_grid(int num_ctx, int cap) { return static_cast<unsigned>(num_ctx < cap ? num_ctx : cap); }
+
+// encode workspace: empty for the gather path; the sort buffers when the batch is
+// large enough for grouping by context to pay off
+struct EncPlan {
+    bool sorted;
+    SortArgs s;
+    size_t off_hist, off_total, off_base, off_perm, off_pos, off_res, bytes;
+};
+
+EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
+    EncPlan p{};
+    p.bytes = 256;
+    p.sorted = nq >= (1 << 16) && nq >= 4 * static_cast<int64_t>(num_ctx) && nq <= 0x7fffffff;
+    if (!p.sorted) return p;
+    const int64_t C = num_ctx > 0 ? num_ctx : 1;
+    int shift = 0;
+    while ((C + (int64_t{1} << shift) - 1) >> shift > kSortMaxBins) ++shift;
+    p.s.bin_shift = shift;
+    p.s.nb = static_cast<int>((C + (int64_t{1} << shift) - 1) >> shift) + 1;
+    // about 256 count / scatter blocks of at least 16k queries: few histogram rows to scan
+    int64_t blocks = (nq + 16383) / 16384;
+    if (blocks > 256) blocks = 256;
+    const int64_t qc = (nq + blocks - 1) / blocks;
+    p.s.qc = qc;
+    p.s.blocks = static_cast<int>((nq + qc - 1) / qc);
+    size_t o = 0;
+    p.off_hist = o;
+    o = align256(o + sizeof(int32_t) * static_cast<size_t>(p.s.blocks) * p.s.nb);
+    p.off_total = o;
+    o = align256(o + sizeof(int32_t) * p.s.nb);
+    p.off_base = o;
+    o = align256(o + sizeof(int32_t) * p.s.nb);
+    p.off_perm = o;
+    o = align256(o + sizeof(int2) * static_cast<size_t>(nq));
+    p.s.direct = nq <= kDirectMaxQueries;
+    p.off_pos = o;
+    p.off_res = o;
+    if (!p.s.direct) {
+        o = align256(o + sizeof(int32_t) * static_cast<size_t>(nq));
+        p.off_res = o;
+        o = align256(o + 2 * sizeof(Word2) * static_cast<size_t>(nq));
+    }
+    p.bytes = o > 256 ? o : 256;
+    return p;
+}
 
 }  // namespace
 
@@ -1600,7 +1838,7 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
 
 size_t f2_encode_workspace_bytes(const f2_model* m, int64_t num_queries) {
     if (!m || m->num_ctx < 0 || num_queries < 0) return 0;
-    return 256;  // reserved
+    return encode_workspace(m->num_ctx, num_queries).bytes;
 }
 
 int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x, int32_t x_stride_words,
@@ -1636,7 +1874,25 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     e.qflags = qflags_out;
     const int64_t blocks = (num_queries + kEncThreads - 1) / kEncThreads;
     if (blocks > 0x7fffffff) return F2_EINVAL;
-    hipLaunchKernelGGL(k_encode, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e);
+    EncPlan p = encode_workspace(m->num_ctx, num_queries);
+    if (!p.sorted) {
+        hipLaunchKernelGGL(k_encode, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e);
+        return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
+    }
+    char* ws = static_cast<char*>(workspace);
+    p.s.hist = reinterpret_cast<int32_t*>(ws + p.off_hist);
+    p.s.total = reinterpret_cast<int32_t*>(ws + p.off_total);
+    p.s.base = reinterpret_cast<int32_t*>(ws + p.off_base);
+    p.s.perm = reinterpret_cast<int2*>(ws + p.off_perm);
+    p.s.pos = reinterpret_cast<int32_t*>(ws + p.off_pos);
+    p.s.res = reinterpret_cast<Word2*>(ws + p.off_res);
+    hipLaunchKernelGGL(k_enc_count, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
+    hipLaunchKernelGGL(k_enc_colscan, dim3((p.s.nb + 255) / 256), dim3(256), 0, s, p.s);
+    hipLaunchKernelGGL(k_enc_binscan, dim3(1), dim3(kSortThreads), 0, s, p.s);
+    hipLaunchKernelGGL(k_enc_scatter, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
+    hipLaunchKernelGGL(k_encode_sorted, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
+    if (!p.s.direct)
+        hipLaunchKernelGGL(k_enc_unsort, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 

@@ -267,6 +267,42 @@ def test_encode_grouped_path_random_widths(f2):
     assert (rq == 0).sum() > 1000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 1000 and (rq & oracle.Q_BAD_CTX).any()
 
 
+def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
+    """One query batch through the context-grouped path (whole batch) and the per-query path
+    (slices below its size threshold), against the oracle, with malformed contexts in the
+    model and context ids out of range."""
+    import torch
+    wl = synth.fit_workload(2, num_ctx=40)
+    n_bits = wl.n_bits.copy()
+    row_off = wl.row_off.copy()
+    n_bits[1] = 5000        # too wide
+    row_off[4] += 1         # context 3: segment not a multiple of the row size
+    ref = oracle.fit_batch(wl.rows, row_off, n_bits)
+    model = f2.Model(np.clip(n_bits, 0, oracle.MAX_N))
+    model.n_bits = parity.to_dev(n_bits)
+    model._struct = None
+    nb = f2.f2_fit_workspace_bytes(model.num_ctx)
+    ws = f2.workspace(nb)
+    assert f2.f2_fit_batch(parity.to_dev(wl.rows), wl.rows.size, parity.to_dev(row_off), model, ws, nb) == 0
+    nq, stride = 100_000, 2
+    ctx, x, _ = synth.queries(wl, nq, stride, 0.05, 0.0)
+    rng = np.random.default_rng(41)
+    idx = rng.choice(nq, size=3000, replace=False)
+    ctx[idx[:1000]] = rng.choice(np.array([-1, 40, 12345, -7], np.int32), size=1000)
+    ctx[idx[1000:2000]] = 1
+    ctx[idx[2000:]] = 3
+    rw, rq = oracle.encode_batch(ref, ctx, x, stride)
+    words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x), stride)    # grouped path
+    torch.cuda.synchronize()
+    parity.compare_encode(words, qf, rw, rq)
+    half = nq // 2
+    for a, b in ((0, half), (half, nq)):                                          # per-query path
+        w2, q2 = f2.encode(model, parity.to_dev(ctx[a:b]), parity.to_dev(x[a * stride:b * stride]), stride)
+        torch.cuda.synchronize()
+        parity.compare_encode(w2, q2, rw[a:b], rq[a:b])
+    assert (rq & oracle.Q_BAD_CTX).sum() >= 3000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 1000
+
+
 def _late_pivot_batch(seed, widths, rows_choices):
     """Long contexts whose rows first span a small subspace and only later reveal new
     pivots (one generator added every few hundred rows), with contradictions late."""
