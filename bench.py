@@ -2,17 +2,23 @@
 """Benchmark of the GF(2) fit + encode hot path on one MI355X.
 
 A step is one pass of the whole path over one batch of synthetic input that is
-already resident in HBM: f2_fit_batch over every context (reduce, classify,
-insert, finalize) followed by f2_encode_batch over the query batch against the
-model just fitted.  Default workload: 4,096 contexts of widths 16..96 (+1
-reserved bit), 2(n+1) rows each (468,656 rows, 13.5 MB), 5% contradictory,
-then 1M queries (stride 2 words) with 2% outside the span.
+already resident in HBM: f2_fit_batch over every context (plan, reduce,
+classify, insert, finalize) followed by f2_encode_batch over the query batch
+against the model just fitted.  Default workload: 4,096 contexts of widths
+17..97 (16..96 uniform input bits plus one reserved bit), 2(n+1) rows each
+(468,656 rows, 13.5 MB), 5% contradictory, then 1M queries (stride 2 words)
+with 2% outside the span.
 
 Prints one JSON line.  `value` is fit rows/s over the fit phase of the timed
-steps; encode words/s and per-phase figures are reported beside it.  The
-roofline object describes the phase that takes longer.
+steps; encode words/s and per-phase figures are reported beside it.  Each phase
+is one library call, timed with HIP events on the stream it is enqueued on.
+The roofline object describes the phase that takes longer: its algorithmic HBM
+bytes per call over its average duration, against the 8 TB/s HBM peak, and the
+measured HBM traffic of its kernels from the committed rocprofv3 counter
+summary when that summary was taken on the current kernel source.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -22,29 +28,114 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_20532_amd", "csrc", "f2gpu.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
 
 WORKLOADS = {
-    # name: (fit recipe, num contexts, queries, stride, out-of-span fraction, zipf exponent)
-    "recipe2": (2, 4096, 1_000_000, 2, 0.02, 0.0),
-    "recipe1": (1, 1, 1000, 1, 0.10, 0.0),
-    "recipe3": (3, 80000, 1_000_000, 4, 0.01, 1.1),
-    "recipe4": (4, 64, 0, 1, 0.0, 0.0),
-    "recipe5": (5, 80000, 100_000_000, 4, 0.01, 1.1),
+    # name: (fit recipe, contexts, queries, stride, out-of-span fraction, zipf exponent, description)
+    "recipe2": (2, 4096, 1_000_000, 2, 0.02, 0.0,
+                "fit 4096 contexts, n in [17,97] (16-96 uniform bits + 1 reserved), 2(n+1) rows, 5% contradictory; "
+                "encode 1M uniform queries, stride 2, 2% out of span"),
+    "recipe1": (1, 1, 1000, 1, 0.10, 0.0,
+                "fit 1 context, n=33 (32 uniform bits + 1 reserved), 200 rows; encode 1000 queries, 10% out of span"),
+    "recipe3": (3, 80000, 1_000_000, 4, 0.01, 1.1,
+                "fit 80000 contexts, n in [8,256] geometric (mean 40), lognormal rows (median 30, max 4000), "
+                "x in a random 0.7n-dim subspace, 1% contradictory; encode 1M Zipf(1.1) queries, stride 4"),
+    "recipe4": (4, 64, 0, 1, 0.0, 0.0, "fit 64 contexts, n=4095, 8192 uniform rows each (full rank)"),
+    "recipe5": (5, 80000, 100_000_000, 4, 0.01, 1.1,
+                "encode only: the 80000 maps of the n-in-[8,256] workload, 100M Zipf(1.1) queries, stride 4, "
+                "1% out of span"),
 }
 
 
-def fit_bytes(wl, rank, W):
+def fit_bytes(wl, rank):
     """Algorithmic HBM bytes of one fit: rows, offsets and widths in; basis rows, pivots, maps and scalars out."""
     import numpy as np
     n = wl.n_bits.astype(np.int64)
+    W = (n + 64) // 64 + 2
     rows_in = int(wl.rows.nbytes) + 8 * (wl.num_ctx + 1) + 4 * wl.num_ctx
     out = int((rank.astype(np.int64) * W * 8).sum() + 4 * rank.sum() + (16 * (n + 1)).sum()) + 20 * wl.num_ctx
     return rows_in + out
 
 
-def encode_bytes(nq, stride, table_bytes):
-    """Per query: context id, x words, 128-bit word, flag byte; plus the one-time table build."""
-    return nq * (4 + 8 * stride + 16 + 1) + table_bytes
+def encode_bytes(wl, nq, stride):
+    """Per query: context id, x words, 128-bit word, flag byte; plus every context's map read once."""
+    import numpy as np
+    return nq * (4 + 8 * stride + 16 + 1) + int((16 * (wl.n_bits.astype(np.int64) + 1)).sum())
+
+
+def source_hash():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def load_traffic(workload):
+    """Measured HBM bytes per call of each phase, if the counter summary matches the current source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None, "no counter summary"
+    meta, phases = {}, {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            parts = line.split()
+            if not parts or parts[0].startswith("#"):
+                continue
+            if parts[0] == "phase" and len(parts) >= 5 and parts[1] == workload:
+                phases[parts[2]] = {"bytes": float(parts[3]), "kernels": parts[4].split(",")}
+            elif len(parts) == 2:
+                meta[parts[0]] = parts[1]
+    if meta.get("source_sha256") != source_hash():
+        return None, "kernel source changed since the counters were taken"
+    return phases, None
+
+
+def sub_workload(wl, c0, c1):
+    """Contexts [c0, c1) of a workload as (rows, row_off, n_bits) with rebased offsets."""
+    off = wl.row_off[c0:c1 + 1]
+    return wl.rows[off[0]:off[-1]], off - off[0], wl.n_bits[c0:c1]
+
+
+def cpu_baseline(wl, ctx, x, stride, nq, do_fit):
+    """The oracle (single-threaded C) on a bounded sample of the same workload: context chunks
+    in order, repeated, for about ten seconds of fitting; then about five seconds of encoding the
+    queries that fall into the first chunk of contexts."""
+    import numpy as np
+    import oracle
+    C = wl.num_ctx
+    k = max(1, C // 32)
+    t_fit, rows_fit, c0, first = 0.0, 0, 0, None
+    while t_fit < (10.0 if do_fit else 0.0) or first is None:
+        c1 = min(C, c0 + k)
+        rows, off, nb = sub_workload(wl, c0, c1)
+        t = time.perf_counter()
+        ref = oracle.fit_batch(rows, off, nb)
+        t_fit += time.perf_counter() - t
+        rows_fit += int(wl.m_rows[c0:c1].sum())
+        if first is None:
+            first = (ref, c1)
+        c0 = c1 % C
+    out = {"cores": 1, "kind": "oracle"}
+    if do_fit:
+        out.update(value=rows_fit / t_fit, unit="rows/s",
+                   sample=f"oracle fit of {rows_fit} rows: chunks of {k} consecutive contexts of the workload "
+                          f"({C} contexts, {wl.total_rows} rows), {t_fit:.1f} s")
+    if nq:
+        ref, cn = first
+        sel = np.nonzero(ctx < cn)[0][:200_000]
+        xs = x.reshape(nq, stride)[sel].reshape(-1)
+        t0, reps = time.perf_counter(), 0
+        while True:
+            oracle.encode_batch(ref, ctx[sel], xs, stride)
+            reps += 1
+            if time.perf_counter() - t0 > 5.0:
+                break
+        wps = len(sel) * reps / (time.perf_counter() - t0)
+        enc_sample = f"oracle encode of {len(sel)} queries of the workload (those on contexts 0..{cn - 1}), {reps} repetitions"
+        if do_fit:
+            out["encode_words_per_s"] = wps
+            out["sample"] += "; " + enc_sample
+        else:
+            out.update(value=wps, unit="words/s", sample=enc_sample)
+    return out
 
 
 def main():
@@ -58,19 +149,16 @@ def main():
                     help="only run a plain device-to-device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build measures one GPU only; run with --gpus 1 "
-              "(contexts shard across GPUs with no exchange, see the design notes)", file=sys.stderr)
+        print("bench.py measures one GPU: contexts are independent and would shard across GPUs with no "
+              "exchange, but this build runs and reports a single GPU only; use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
     import torch
 
-    import synth
-    from paper_2608_20532_amd import f2gpu
-
     if args.copy_calibration_mb:
-        # plain copy of a known size: its FETCH_SIZE / WRITE_SIZE readings give the
-        # counter-to-bytes factor used for the roofline traffic figure
+        # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE readings give the
+        # counter-to-bytes factors used for the roofline traffic figure
         nbytes = args.copy_calibration_mb << 20
         src = torch.ones(nbytes // 8, dtype=torch.int64, device="cuda:0")
         dst = torch.empty_like(src)
@@ -80,11 +168,15 @@ def main():
         print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 3}), flush=True)
         return
 
-    recipe, num_ctx, nq, stride, frac, zipf = WORKLOADS[args.workload]
+    import synth
+    from paper_2608_20532_amd import f2gpu
+
+    recipe, num_ctx, nq, stride, frac, zipf, desc = WORKLOADS[args.workload]
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     t0 = time.time()
     wl = synth.fit_workload(recipe, num_ctx=num_ctx)
+    ctx = x = None
     if nq:
         ctx, x, _ = synth.queries(wl, nq, stride, frac, zipf)
     print(f"[bench] generated {args.workload}: {wl.num_ctx} contexts, {wl.total_rows} rows, {nq} queries "
@@ -101,7 +193,7 @@ def main():
         qf = torch.empty(nq, dtype=torch.uint8, device=dev)
         ews = f2gpu.f2_encode_workspace_bytes(model, nq)
         enc_ws = f2gpu.workspace(ews, dev)
-    stream = torch.cuda.current_stream()
+    stream = torch.cuda.current_stream()  # the library enqueues every kernel on this stream
     sptr = stream.cuda_stream
     do_fit = args.workload != "recipe5"
 
@@ -145,50 +237,29 @@ def main():
           file=sys.stderr, flush=True)
 
     rank = model.rank.cpu().numpy()[:wl.num_ctx]
-    W = (wl.n_bits.astype(np.int64) + 64) // 64 + 2
-    fb = fit_bytes(wl, rank, W)
-    n = wl.n_bits.astype(np.int64)
-    hw = ((n + 1 - rank) + 63) // 64
-    table_bytes = int(((n + 1) * (2 + hw) * 8).sum() + (rank * W * 8).sum())
-    eb = encode_bytes(nq, stride, table_bytes) if nq else 0
-    rows_per_s = wl.total_rows / (fit_ms * 1e-3) if do_fit else None
-    words_per_s = nq / (enc_ms * 1e-3) if nq else None
     phases = {}
     if do_fit:
-        phases["fit"] = {"ms": fit_ms, "bytes": fb, "GBps": fb / (fit_ms * 1e-3) / 1e9}
+        fb = fit_bytes(wl, rank)
+        phases["fit"] = {"call": "f2_fit_batch", "ms": fit_ms, "bytes": fb, "GBps": fb / (fit_ms * 1e-3) / 1e9}
     if nq:
-        phases["encode"] = {"ms": enc_ms, "bytes": eb, "GBps": eb / (enc_ms * 1e-3) / 1e9}
+        eb = encode_bytes(wl, nq, stride)
+        phases["encode"] = {"call": "f2_encode_batch", "ms": enc_ms, "bytes": eb,
+                            "GBps": eb / (enc_ms * 1e-3) / 1e9}
     dom = max(phases, key=lambda k: phases[k]["ms"])
-    ach = phases[dom]["GBps"]
+    traffic, why = load_traffic(args.workload)
+    tr = traffic.get(dom) if traffic else None
+    roof = {"bound": "hbm", "kernel": phases[dom]["call"], "achieved": phases[dom]["GBps"], "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": phases[dom]["GBps"] / HBM_PEAK_GBS,
+            "traffic": tr["bytes"] if tr else None,
+            "algorithmic_bytes": phases[dom]["bytes"], "avg_ms": phases[dom]["ms"]}
+    if tr:
+        roof["kernels"] = tr["kernels"]
+    else:
+        roof["traffic_note"] = why or f"no counters for the {dom} phase of this workload"
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        import oracle
-        # bounded sample: the oracle on the same workload (whole fit for small recipes, else a prefix)
-        t = time.perf_counter()
-        if do_fit:
-            nsub = wl.num_ctx if wl.total_rows <= 2_000_000 else 4000
-            sub = wl if nsub == wl.num_ctx else synth.fit_workload(recipe, num_ctx=nsub)
-            ref = oracle.fit_batch(sub.rows, sub.row_off, sub.n_bits)
-            fit_s = time.perf_counter() - t
-            cpu_rows = sub.total_rows / fit_s
-            sample = f"oracle fit of {sub.num_ctx} contexts ({sub.total_rows} rows) of the same workload"
-            cpu = {"value": cpu_rows, "unit": "rows/s", "cores": 1, "kind": "oracle", "sample": sample}
-            if nq:
-                qs = min(nq, 200_000)
-                ref_full = ref if nsub == wl.num_ctx else oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
-                t = time.perf_counter()
-                oracle.encode_batch(ref_full, ctx[:qs], x[:qs * stride], stride)
-                cpu["encode_words_per_s"] = qs / (time.perf_counter() - t)
-                cpu["sample"] += f"; oracle encode of the first {qs} queries"
-        else:
-            ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
-            qs = 1_000_000
-            t = time.perf_counter()
-            oracle.encode_batch(ref, ctx[:qs], x[:qs * stride], stride)
-            cpu = {"value": qs / (time.perf_counter() - t), "unit": "words/s", "cores": 1, "kind": "oracle",
-                   "sample": f"oracle encode of the first {qs} queries"}
-
+    cpu = None if args.no_cpu_baseline else cpu_baseline(wl, ctx, x, stride, nq, do_fit)
+    rows_per_s = wl.total_rows / (fit_ms * 1e-3) if do_fit else None
+    words_per_s = nq / (enc_ms * 1e-3) if nq else None
     out = {
         "metric": "GF(2) fit rows/sec and encoded words/sec on 1 MI355X; % of HBM/int-op roofline",
         "value": rows_per_s if do_fit else words_per_s,
@@ -202,13 +273,12 @@ def main():
         "vs_baseline": None,
         "dtype": "u64",
         "data": "synthetic",
-        "config": {"workload": args.workload, "contexts": wl.num_ctx, "rows": wl.total_rows, "queries": nq,
-                   "query_stride_words": stride, "fit_in_step": do_fit},
+        "config": {"workload": desc, "name": args.workload, "contexts": wl.num_ctx, "rows": wl.total_rows,
+                   "queries": nq, "query_stride_words": stride, "fit_in_step": do_fit},
         "fit_rows_per_s": rows_per_s,
         "encode_words_per_s": words_per_s,
         "phases": phases,
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": ach / HBM_PEAK_GBS, "traffic": None},
+        "roofline": roof,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
