@@ -175,11 +175,11 @@ __device__ void write_bad_context(const FitArgs& a, const CtxDesc& ds) {
 // A class kernel with G workgroups deals its list out in stripes of G entries,
 // alternating direction from stripe to stripe, so that every workgroup gets a
 // similar share of the work and the longest contexts start first.  The sort is
-// a counting sort over (class, cost bucket) bins in three kernels (per-block
-// histograms, one scan, a scatter) with no device-wide atomics: on a chip of
-// eight dies those serialise far from the compute units.
+// a counting sort over (class, cost bucket) bins in two kernels (per-block
+// histograms; a scatter that scans them) with no device-wide atomics: on a chip
+// of eight dies those serialise far from the compute units.
 // Workspace (int32): [0, 5) list offsets per class, [16, 16 + C) the lists,
-// then C sort keys, kPlanBins bin bases and a kPlanBins histogram per plan block.
+// then C sort keys and a kPlanBins histogram per plan block.
 // ---------------------------------------------------------------------------
 constexpr int kRegMaxFW = 3;
 constexpr int kPivMaxFW = 8;
@@ -213,7 +213,6 @@ struct PlanView {
     int32_t* cls_off;  // [kNumCls + 1]
     int32_t* order;    // [C]
     int32_t* key;      // [C]
-    int32_t* bin_base; // [kPlanBins]
     int32_t* hist;     // [blocks][kPlanBins]
 };
 
@@ -222,8 +221,7 @@ __device__ __forceinline__ PlanView plan_view(const FitArgs& a) {
     v.cls_off = a.plan;
     v.order = a.plan + kPlanHead;
     v.key = v.order + a.num_ctx;
-    v.bin_base = v.key + a.num_ctx;
-    v.hist = v.bin_base + kPlanBins;
+    v.hist = v.key + a.num_ctx;
     return v;
 }
 
@@ -250,16 +248,19 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_count(FitArgs a) {
     P.hist[static_cast<int64_t>(blockIdx.x) * kPlanBins + tid] = sBin[tid];
 }
 
-// (2) one workgroup: per bin, exclusive prefix over the blocks; then the bin bases
-__global__ __launch_bounds__(kPlanThreads) void k_plan_scan(FitArgs a, int blocks) {
+// (2) scatter.  Thread b of every block sums bin b over all blocks (its total) and
+// over the blocks before this one; a block scan of the totals gives the bin bases.
+// List position = bin base + earlier blocks' count + rank within the block.
+__global__ __launch_bounds__(kPlanThreads) void k_plan_scatter(FitArgs a, int blocks) {
+    __shared__ int sBin[kPlanBins];
     __shared__ int sWave[kPlanThreads / 64];
     const PlanView P = plan_view(a);
     const int tid = threadIdx.x, lane = tid & 63;
-    int total = 0;
+    const int g0 = static_cast<int>(blockIdx.x);
+    int total = 0, before = 0;
     for (int g = 0; g < blocks; ++g) {
-        int32_t* h = P.hist + static_cast<int64_t>(g) * kPlanBins + tid;
-        const int v = *h;
-        *h = total;
+        const int v = P.hist[static_cast<int64_t>(g) * kPlanBins + tid];
+        before += g < g0 ? v : 0;
         total += v;
     }
     int x = total;
@@ -272,19 +273,13 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_scan(FitArgs a, int block
     int base = 0;
     for (int w = 0; w < (tid >> 6); ++w) base += sWave[w];
     const int excl = base + x - total;
-    P.bin_base[tid] = excl;
-    if (tid % kBuckets == 0) P.cls_off[tid / kBuckets] = excl;
-    if (tid == kPlanThreads - 1) P.cls_off[kNumCls] = excl + total;
-}
-
-// (3) scatter: list position = bin base + earlier blocks' count + rank within the block
-__global__ __launch_bounds__(kPlanThreads) void k_plan_scatter(FitArgs a) {
-    __shared__ int sBin[kPlanBins];
-    const PlanView P = plan_view(a);
-    const int tid = threadIdx.x;
-    sBin[tid] = P.bin_base[tid] + P.hist[static_cast<int64_t>(blockIdx.x) * kPlanBins + tid];
+    if (g0 == 0) {
+        if (tid % kBuckets == 0) P.cls_off[tid / kBuckets] = excl;
+        if (tid == kPlanThreads - 1) P.cls_off[kNumCls] = excl + total;
+    }
+    sBin[tid] = excl + before;
     __syncthreads();
-    const int64_t c = static_cast<int64_t>(blockIdx.x) * kPlanThreads + tid;
+    const int64_t c = static_cast<int64_t>(g0) * kPlanThreads + tid;
     if (c < a.num_ctx) {
         const int k = P.key[c];
         if (k >= 0) P.order[atomicAdd(&sBin[k], 1)] = static_cast<int32_t>(c);
@@ -883,7 +878,7 @@ template <int NW>
 __global__ __launch_bounds__(64 * NW) void k_fit_piv(FitArgs a) {
     __shared__ PivShared S;
     for (int i = 0;; ++i) {
-        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, NW > 1 ? kClsPivLong : kClsPiv, i));
+        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsPiv, i));
         if (c < 0) break;
         const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
         switch (feat_words(ds.n)) {
@@ -942,24 +937,33 @@ __device__ __forceinline__ void unstage_rows(const uint64_t (*src)[kMaxW], uint6
     }
 }
 
-__global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
-    __shared__ uint64_t sRow[kLargeRows][kMaxW];
+struct LargeShared {
+    uint64_t sRow[kLargeRows][kMaxW];
     // one buffer, two uses: two halves of staged retained rows (blocked phase), map columns (full-rank phase)
-    __shared__ uint64_t sBuf[2 * kLargeRows * kMaxW];
-    uint64_t (*sZ)[2] = reinterpret_cast<uint64_t (*)[2]>(sBuf);
-    __shared__ uint64_t sPmask[64];
-    __shared__ uint64_t sNew[kLargeRows][kMaxW];  // the block's new rows, in insertion order
-    __shared__ int sNewRow[kLargeRows];  // block row of the k-th new pivot
-    __shared__ int sNewPiv[kLargeRows];  // its pivot
-    __shared__ int sNumNew, sContra;
-    __shared__ long long sFirst, sFirstCons;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    uint64_t sBuf[2 * kLargeRows * kMaxW];
+    uint64_t sPmask[64];
+    uint64_t sNew[kLargeRows][kMaxW];  // the block's new rows, in insertion order
+    int sNewRow[kLargeRows];           // block row of the k-th new pivot
+    int sNewPiv[kLargeRows];           // its pivot
+    int sNumNew, sContra;
+    long long sFirst, sFirstCons;
+};
 
-    for (int i = 0;; ++i) {
-      const int cc = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsLarge, i));
-      if (cc < 0) break;
+__device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& ds, LargeShared& L) {
+    uint64_t (&sRow)[kLargeRows][kMaxW] = L.sRow;
+    uint64_t* sBuf = L.sBuf;
+    uint64_t (*sZ)[2] = reinterpret_cast<uint64_t (*)[2]>(L.sBuf);
+    uint64_t* sPmask = L.sPmask;
+    uint64_t (&sNew)[kLargeRows][kMaxW] = L.sNew;
+    int* sNewRow = L.sNewRow;
+    int* sNewPiv = L.sNewPiv;
+    int& sNumNew = L.sNumNew;
+    int& sContra = L.sContra;
+    long long& sFirst = L.sFirst;
+    long long& sFirstCons = L.sFirstCons;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    {
       {
-        const CtxDesc ds = readlane_desc(load_desc(a, cc), 0);
         const int c = ds.c;
         const int n = ds.n;
         const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
@@ -1301,6 +1305,35 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_large(FitArgs a) {
         }
         __syncthreads();
       }
+    }
+}
+
+// contexts of class 2 (fw <= 8, long: pivot-indexed LDS basis, kPivWaves wavefronts)
+// and class 3 (fw > 8: large-context path) share one launch: both run 8
+// wavefronts and are limited to one workgroup per compute unit, so the union of
+// their shared memory costs no occupancy
+union WideShared {
+    PivShared piv;
+    LargeShared large;
+};
+
+__global__ __launch_bounds__(kLargeThreads) void k_fit_wide(FitArgs a) {
+    __shared__ WideShared U;
+    for (int i = 0;; ++i) {
+        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsPivLong, i));
+        if (c < 0) break;
+        const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
+        switch (feat_words(ds.n)) {
+            case 1: fit_ctx_piv<1, kPivWaves>(a, ds, U.piv); break;
+            case 2: fit_ctx_piv<2, kPivWaves>(a, ds, U.piv); break;
+            case 3: case 4: fit_ctx_piv<4, kPivWaves>(a, ds, U.piv); break;
+            default: fit_ctx_piv<8, kPivWaves>(a, ds, U.piv); break;
+        }
+    }
+    for (int i = 0;; ++i) {
+        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsLarge, i));
+        if (c < 0) break;
+        fit_ctx_large(a, readlane_desc(load_desc(a, c), 0), U.large);
     }
 }
 
@@ -1786,8 +1819,7 @@ int f2_fit_layout(const int32_t* n_bits_host, int32_t num_ctx, int64_t* basis_of
 size_t f2_fit_workspace_bytes(int32_t num_ctx) {
     if (num_ctx < 0) return 0;
     const size_t blocks = (static_cast<size_t>(num_ctx) + kPlanThreads - 1) / kPlanThreads;
-    return align256(sizeof(int32_t) *
-                    (kPlanHead + 2 * static_cast<size_t>(num_ctx) + kPlanBins * (1 + blocks)));
+    return align256(sizeof(int32_t) * (kPlanHead + 2 * static_cast<size_t>(num_ctx) + kPlanBins * blocks));
 }
 
 int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m,
@@ -1827,12 +1859,10 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     // each class kernel keeps about as many workgroups as fit on the chip at once
     const int plan_blocks = static_cast<int>((static_cast<int64_t>(C) + kPlanThreads - 1) / kPlanThreads);
     hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
-    hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kPlanThreads), 0, s, a, plan_blocks);
-    hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
+    hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
     hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid(C, 4096)), dim3(64), 0, s, a);
     hipLaunchKernelGGL(k_fit_piv<1>, dim3(fit_grid(C, 1024)), dim3(64), 0, s, a);
-    hipLaunchKernelGGL(k_fit_piv<kPivWaves>, dim3(fit_grid(C, 256)), dim3(64 * kPivWaves), 0, s, a);
-    hipLaunchKernelGGL(k_fit_large, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
+    hipLaunchKernelGGL(k_fit_wide, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 
