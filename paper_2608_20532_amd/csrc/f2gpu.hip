@@ -306,6 +306,14 @@ __device__ __forceinline__ int class_ctx(const FitArgs& a, int cls, int i) {
 // columns than basis rows is encoded by reducing phi with the basis itself.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ bool has_parity_rows(int d, int rank) { return d - rank <= rank; }
+// orders a wavefront's own LDS accesses: used where a wavefront works alone on
+// its LDS region, so that no workgroup barrier couples it to the others
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // ---------------------------------------------------------------------------
 // register-basis fit (fw <= 3): one wavefront per context.  Lane s of register
 // set k holds retained row 64k + s (fw + 2 words and its pivot); the rows of
@@ -348,7 +356,7 @@ template <int FW>
 __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec, int16_t* sPos) {
     constexpr int W = FW + F2_Y_WORDS;
     constexpr int NS = FW;  // register sets: d <= 64 FW retained rows
-    const int lane = threadIdx.x;
+    const int lane = threadIdx.x & 63;
     const int c = ds.c, n = ds.n, d = n + 1;
     const int64_t m = ds.m;
     const uint64_t* R = a.rows + ds.row0;
@@ -512,13 +520,13 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
         }
         if (changed && b0 + 64 < m) {
             store_mirror();
-            __syncthreads();
+            wave_sync();
         }
     }
 
     // outputs: basis rows and pivots in descending priority, canonical map, scalars
     store_mirror();
-    __syncthreads();
+    wave_sync();
     const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
 #pragma unroll
     for (int k = 0; k < NS; ++k) {
@@ -581,21 +589,38 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
         a.first_contra[c] = first;
         a.ctx_flags[c] = ncontra ? F2_CTX_CONTRADICTION : 0u;
     }
-    __syncthreads();
+    wave_sync();
 }
 
-__global__ __launch_bounds__(64) void k_fit_reg(FitArgs a) {
-    __shared__ __align__(16) uint64_t sRec[64 * kRegMaxFW * kRecWords];
-    __shared__ int16_t sPos[64 * kRegMaxFW];
-    for (int i = 0;; ++i) {
-        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsReg, i));
+// One workgroup of kRegWaves wavefronts per compute unit, each wavefront fitting
+// its own contexts in its own LDS region.  The workgroup's share of the class
+// list (dealt in snake order, so shares carry similar work) starts with one
+// context per wavefront in snake order over the four SIMDs (wavefront w runs on
+// SIMD w mod 4), largest first; then wavefronts take the next context of the
+// share as they finish, through a counter in LDS.
+constexpr int kRegWaves = 16;
+
+__global__ __launch_bounds__(64 * kRegWaves) void k_fit_reg(FitArgs a) {
+    __shared__ __align__(16) uint64_t sRec[kRegWaves][64 * kRegMaxFW * kRecWords];
+    __shared__ int16_t sPos[kRegWaves][64 * kRegMaxFW];
+    __shared__ int sNext;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    if (tid == 0) sNext = kRegWaves;
+    __syncthreads();
+    const int r = wave >> 2, simd = wave & 3;
+    int k = 4 * r + ((r & 1) ? 3 - simd : simd);
+    for (;;) {
+        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsReg, k));
         if (c < 0) break;
         const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
         switch (feat_words(ds.n)) {
-            case 1: fit_ctx_reg<1>(a, ds, sRec, sPos); break;
-            case 2: fit_ctx_reg<2>(a, ds, sRec, sPos); break;
-            default: fit_ctx_reg<3>(a, ds, sRec, sPos); break;
+            case 1: fit_ctx_reg<1>(a, ds, sRec[wave], sPos[wave]); break;
+            case 2: fit_ctx_reg<2>(a, ds, sRec[wave], sPos[wave]); break;
+            default: fit_ctx_reg<3>(a, ds, sRec[wave], sPos[wave]); break;
         }
+        int nk = 0;
+        if (lane == 0) nk = atomicAdd(&sNext, 1);
+        k = __builtin_amdgcn_readfirstlane(nk);
     }
 }
 
@@ -1860,7 +1885,7 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     const int plan_blocks = static_cast<int>((static_cast<int64_t>(C) + kPlanThreads - 1) / kPlanThreads);
     hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
     hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
-    hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid(C, 4096)), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid((C + kRegWaves - 1) / kRegWaves, 256)), dim3(64 * kRegWaves), 0, s, a);
     hipLaunchKernelGGL(k_fit_piv<1>, dim3(fit_grid(C, 1024)), dim3(64), 0, s, a);
     hipLaunchKernelGGL(k_fit_wide, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
