@@ -355,24 +355,31 @@ constexpr int kRecWords = 6;  // LDS record: fw feature words, 2 output words, p
 template <int FW>
 __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec, int16_t* sPos) {
     constexpr int W = FW + F2_Y_WORDS;
-    constexpr int NS = FW;  // register sets: d <= 64 FW retained rows
+    constexpr int NB = kLongRows / 64;  // blocks of a context in this class
     const int lane = threadIdx.x & 63;
     const int c = ds.c, n = ds.n, d = n + 1;
-    const int64_t m = ds.m;
+    const int64_t m = ds.m;  // at most kLongRows
     const uint64_t* R = a.rows + ds.row0;
     const uint64_t tmask = top_mask(n, FW);
     const int cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
+    const uint64_t lane_lt = (1ull << lane) - 1;
 
-    for (int j = lane; j < d; j += 64) sPos[j] = -1;
-    uint64_t bf[NS][FW], by0[NS], by1[NS];
-    int bp[NS];
+    // block b's rows in register set b, one per lane; every row is loaded up front
+    uint64_t f[NB][FW], y0[NB], y1[NB];
+    int bp[NB];         // pivot of this lane's row, where the row is a basis row
+    uint64_t piv[NB];   // lanes of set b that hold basis rows (uniform)
 #pragma unroll
-    for (int k = 0; k < NS; ++k) {
+    for (int b = 0; b < NB; ++b) {
+        const int64_t i = 64 * b + lane;
+        const bool valid = i < m;
 #pragma unroll
-        for (int w = 0; w < FW; ++w) bf[k][w] = 0;
-        by0[k] = by1[k] = 0;
-        bp[k] = 0;
+        for (int w = 0; w < FW; ++w) f[b][w] = valid ? R[i * W + w] : 0ull;
+        f[b][FW - 1] &= tmask;
+        y0[b] = valid ? R[i * W + FW] : 0ull;
+        y1[b] = valid ? R[i * W + FW + 1] : 0ull;
+        bp[b] = 0;
+        piv[b] = 0;
     }
     uint64_t pm[FW];  // pivot columns (uniform)
 #pragma unroll
@@ -380,96 +387,87 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
     int rank = 0, ncontra = 0;
     int64_t first = -1;
 
-    auto store_mirror = [&]() {
+    // dense copy of the basis rows (record = fw words, 2 output words, pivot) for
+    // the broadcast reads of the block reduce; sPos[p] = record of pivot p
+    auto store_mirror = [&](int nsets, bool positions) {
+        int base = 0;
 #pragma unroll
-        for (int k = 0; k < NS; ++k) {
-            const int s = 64 * k + lane;
-            if (s < rank) {
-                uint64_t* rec = sRec + s * kRecWords;
+        for (int k = 0; k < NB; ++k) {
+            if (k < nsets) {
+                if ((piv[k] >> lane) & 1ull) {
+                    const int s = base + __popcll(piv[k] & lane_lt);
+                    uint64_t* rec = sRec + s * kRecWords;
 #pragma unroll
-                for (int w = 0; w < FW; ++w) rec[w] = bf[k][w];
-                rec[FW] = by0[k];
-                rec[FW + 1] = by1[k];
-                rec[W] = static_cast<uint64_t>(bp[k]);
+                    for (int w = 0; w < FW; ++w) rec[w] = f[k][w];
+                    rec[FW] = y0[k];
+                    rec[FW + 1] = y1[k];
+                    rec[W] = static_cast<uint64_t>(bp[k]);
+                    if (positions) sPos[bp[k]] = static_cast<int16_t>(s);
+                }
+                base += __popcll(piv[k]);
             }
         }
     };
 
-    for (int64_t b0 = 0; b0 < m; b0 += 64) {
-        const int64_t i = b0 + lane;
-        const bool valid = i < m;
-        uint64_t f[FW], y0 = 0, y1 = 0;
 #pragma unroll
-        for (int w = 0; w < FW; ++w) f[w] = 0;
-        if (valid) {
-            const uint64_t* row = R + i * W;
+    for (int b = 0; b < NB; ++b) {
+        if (64 * b >= m) break;
+        const bool valid = 64 * b + lane < m;
+        // (1) reduce against the basis of the earlier blocks: it is fully reduced,
+        //     so the row's own (unreduced) bits at the pivot columns select the
+        //     records to add; the selection masks do not depend on one another
+        if (rank > 0) {
+            uint64_t f0[FW];
 #pragma unroll
-            for (int w = 0; w < FW; ++w) f[w] = row[w];
-            y0 = row[FW];
-            y1 = row[FW + 1];
-            f[FW - 1] &= tmask;
-        }
-
-        // (1) reduce against the retained basis: it is fully reduced, so the
-        //     row's own (unreduced) bits at the pivot columns select the rows to
-        //     add; the selection masks do not depend on one another
-        uint64_t f0[FW];
+            for (int w = 0; w < FW; ++w) f0[w] = f[b][w];
+            constexpr int U = FW >= 3 ? 1 : FW == 2 ? 2 : 4;  // records read ahead (register budget)
+            int s = 0;
+            for (; s + U <= rank; s += U) {
+                uint64_t rv[U][W];
+                int pv[U];
 #pragma unroll
-        for (int w = 0; w < FW; ++w) f0[w] = f[w];
-        int s = 0;
-        for (; s + 4 <= rank; s += 4) {
-            uint64_t rv[4][W];
-            int pv[4];
+                for (int u = 0; u < U; ++u) {
+                    const uint64_t* rec = sRec + (s + u) * kRecWords;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const uint64_t* rec = sRec + (s + u) * kRecWords;
-#pragma unroll
-                for (int w = 0; w < W; ++w) rv[u][w] = rec[w];
-                pv[u] = static_cast<int>(rec[W]);
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const uint32_t mm = bit_mask(word_at<FW>(f0, pv[u] >> 6), pv[u] & 63);
-#pragma unroll
-                for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, rv[u][w]);
-                y0 = xor_and(y0, mm, rv[u][FW]);
-                y1 = xor_and(y1, mm, rv[u][FW + 1]);
-            }
-        }
-        for (; s < rank; ++s) {
-            const uint64_t* rec = sRec + s * kRecWords;
-            const int p = static_cast<int>(rec[W]);
-            const uint32_t mm = bit_mask(word_at<FW>(f0, p >> 6), p & 63);
-#pragma unroll
-            for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, rec[w]);
-            y0 = xor_and(y0, mm, rec[FW]);
-            y1 = xor_and(y1, mm, rec[FW + 1]);
-        }
-
-        // (2) in-block elimination in stream order
-        uint64_t pending = __ballot(valid);
-        bool changed = false;
-        while (pending) {
-            uint64_t any = f[0];
-#pragma unroll
-            for (int w = 1; w < FW; ++w) any |= f[w];
-            const uint64_t nz = __ballot(any != 0) & pending;
-            const int j = nz ? ffs64(nz) : 64;
-            const uint64_t before = (j >= 64) ? pending : (pending & ((1ull << j) - 1));
-            if (before) {
-                // zero-feature residuals: redundant, or contradictory when the output is nonzero
-                const uint64_t cm = __ballot((y0 | y1) != 0) & before;
-                if (cm) {
-                    if (ncontra == 0) first = b0 + ffs64(cm);
-                    ncontra += __popcll(cm);
+                    for (int w = 0; w < W; ++w) rv[u][w] = rec[w];
+                    pv[u] = static_cast<int>(rec[W]);
                 }
-                pending &= ~before;
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const uint32_t mm = bit_mask(word_at<FW>(f0, pv[u] >> 6), pv[u] & 63);
+#pragma unroll
+                    for (int w = 0; w < FW; ++w) f[b][w] = xor_and(f[b][w], mm, rv[u][w]);
+                    y0[b] = xor_and(y0[b], mm, rv[u][FW]);
+                    y1[b] = xor_and(y1[b], mm, rv[u][FW + 1]);
+                }
             }
-            if (j >= 64) break;
+            for (; s < rank; ++s) {
+                const uint64_t* rec = sRec + s * kRecWords;
+                const int p = static_cast<int>(rec[W]);
+                const uint32_t mm = bit_mask(word_at<FW>(f0, p >> 6), p & 63);
+#pragma unroll
+                for (int w = 0; w < FW; ++w) f[b][w] = xor_and(f[b][w], mm, rec[w]);
+                y0[b] = xor_and(y0[b], mm, rec[FW]);
+                y1[b] = xor_and(y1[b], mm, rec[FW + 1]);
+            }
+        }
+
+        // (2) elimination in stream order: the earliest row with a nonzero
+        //     feature residual becomes a basis row where it stands; its pivot is
+        //     cleared from the later rows of the block and from the basis rows
+        //     of this and the earlier blocks (the basis stays fully reduced)
+        uint64_t pending = __ballot(valid);
+        for (;;) {
+            uint64_t any = f[b][0];
+#pragma unroll
+            for (int w = 1; w < FW; ++w) any |= f[b][w];
+            const uint64_t nz = __ballot(any != 0) & pending;
+            if (!nz) break;
+            const int j = ffs64(nz);
             uint64_t F[FW];
 #pragma unroll
-            for (int w = 0; w < FW; ++w) F[w] = readlane64(f[w], j);
-            const uint64_t Y0 = readlane64(y0, j), Y1 = readlane64(y1, j);
+            for (int w = 0; w < FW; ++w) F[w] = readlane64(f[b][w], j);
+            const uint64_t Y0 = readlane64(y0[b], j), Y1 = readlane64(y1[b], j);
             // pivot: highest-priority set feature bit (x_{n-1} .. x_0, then the constant)
             int p = -1;
 #pragma unroll
@@ -479,59 +477,53 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
             }
             if (p < 0) p = n;
             const int pw = p >> 6, pb = p & 63;
-            {  // rows of the block that hold bit p (rows no longer pending are never read again)
-                const uint32_t mm = bit_mask(word_at<FW>(f, pw), pb);
+            {  // this block: every row holding bit p except the new basis row itself
+                const uint32_t mm = bit_mask(word_at<FW>(f[b], pw), pb) & (lane == j ? 0u : ~0u);
 #pragma unroll
-                for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, F[w]);
-                y0 = xor_and(y0, mm, Y0);
-                y1 = xor_and(y1, mm, Y1);
+                for (int w = 0; w < FW; ++w) f[b][w] = xor_and(f[b][w], mm, F[w]);
+                y0[b] = xor_and(y0[b], mm, Y0);
+                y1[b] = xor_and(y1[b], mm, Y1);
             }
 #pragma unroll
-            for (int k = 0; k < NS; ++k) {  // clear p from the retained rows
-                if (64 * k < rank) {
-                    const uint32_t mm = bit_mask(word_at<FW>(bf[k], pw), pb);
+            for (int k = 0; k < NB; ++k) {  // earlier blocks: only their basis rows are nonzero
+                if (k < b && piv[k]) {
+                    const uint32_t mm = bit_mask(word_at<FW>(f[k], pw), pb);
 #pragma unroll
-                    for (int w = 0; w < FW; ++w) bf[k][w] = xor_and(bf[k][w], mm, F[w]);
-                    by0[k] = xor_and(by0[k], mm, Y0);
-                    by1[k] = xor_and(by1[k], mm, Y1);
+                    for (int w = 0; w < FW; ++w) f[k][w] = xor_and(f[k][w], mm, F[w]);
+                    y0[k] = xor_and(y0[k], mm, Y0);
+                    y1[k] = xor_and(y1[k], mm, Y1);
                 }
             }
-            {  // insert at slot `rank`
-                const int ks = rank >> 6;
-                const bool me = lane == (rank & 63);
-#pragma unroll
-                for (int k = 0; k < NS; ++k) {
-                    if (k == ks && me) {
-#pragma unroll
-                        for (int w = 0; w < FW; ++w) bf[k][w] = F[w];
-                        by0[k] = Y0;
-                        by1[k] = Y1;
-                        bp[k] = p;
-                    }
-                }
-            }
+            if (lane == j) bp[b] = p;
 #pragma unroll
             for (int w = 0; w < FW; ++w)
                 if (w == pw) pm[w] |= 1ull << pb;
-            if (lane == 0) sPos[p] = static_cast<int16_t>(rank);
-            ++rank;
+            piv[b] |= 1ull << j;
             pending &= ~(1ull << j);
-            changed = true;
+            ++rank;
         }
-        if (changed && b0 + 64 < m) {
-            store_mirror();
+        // (3) every other row of the block now has zero features: redundant, or
+        //     contradictory when its output is nonzero (Eq. 8)
+        const uint64_t cm = __ballot(valid && !((piv[b] >> lane) & 1ull) && (y0[b] | y1[b]) != 0);
+        if (cm) {
+            if (ncontra == 0) first = 64 * b + ffs64(cm);
+            ncontra += __popcll(cm);
+        }
+        if (piv[b] && 64 * (b + 1) < m) {
+            store_mirror(b + 1, false);
             wave_sync();
         }
     }
 
     // outputs: basis rows and pivots in descending priority, canonical map, scalars
-    store_mirror();
+    for (int j = lane; j < d; j += 64) sPos[j] = -1;
+    wave_sync();
+    store_mirror(NB, true);
     wave_sync();
     const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
 #pragma unroll
-    for (int k = 0; k < NS; ++k) {
-        const int s = 64 * k + lane;
-        if (s < rank) {
+    for (int k = 0; k < NB; ++k) {
+        if ((piv[k] >> lane) & 1ull) {
             const int p = bp[k];
             int kout = rank - 1;
             if (p != n) {  // pivots of higher priority: x bits above p
@@ -547,9 +539,9 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
             }
             uint64_t* out = a.basis + bo + static_cast<int64_t>(kout) * W;
 #pragma unroll
-            for (int w = 0; w < FW; ++w) out[w] = bf[k][w];
-            out[FW] = by0[k];
-            out[FW + 1] = by1[k];
+            for (int w = 0; w < FW; ++w) out[w] = f[k][w];
+            out[FW] = y0[k];
+            out[FW + 1] = y1[k];
             a.pivots[po + kout] = p;
         }
     }
@@ -558,7 +550,7 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
         a.maps[mo + 2 * j] = sl >= 0 ? sRec[sl * kRecWords + FW] : 0ull;
         a.maps[mo + 2 * j + 1] = sl >= 0 ? sRec[sl * kRecWords + FW + 1] : 0ull;
     }
-    // parity-check rows of the free columns (sRec holds the final rows, sPos their slots)
+    // parity-check rows of the free columns (sRec holds the final rows, sPos their records)
     uint64_t* H = a.tables + bo;
     int slot[FW];
 #pragma unroll
@@ -569,17 +561,18 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
     for (int w = 0; w < FW; ++w) {
         uint64_t fr = rows ? ~pm[w] & (w == FW - 1 ? tmask : ~0ull) : 0ull;
         while (fr) {
-            const int f = 64 * w + ffs64(fr);
+            const int fc = 64 * w + ffs64(fr);
             fr &= fr - 1;
-            uint64_t hw_[FW];
+            uint64_t hv[FW];
 #pragma unroll
             for (int v = 0; v < FW; ++v) {
-                const bool has = slot[v] >= 0 && ((sRec[(slot[v] < 0 ? 0 : slot[v]) * kRecWords + w] >> (f & 63)) & 1ull);
-                hw_[v] = __ballot(has) | (v == w ? (1ull << (f & 63)) : 0ull);
+                const bool has =
+                    slot[v] >= 0 && ((sRec[(slot[v] < 0 ? 0 : slot[v]) * kRecWords + w] >> (fc & 63)) & 1ull);
+                hv[v] = __ballot(has) | (v == w ? (1ull << (fc & 63)) : 0ull);
             }
 #pragma unroll
             for (int v = 0; v < FW; ++v)
-                if (lane == v) H[static_cast<int64_t>(i) * FW + v] = hw_[v];
+                if (lane == v) H[static_cast<int64_t>(i) * FW + v] = hv[v];
             ++i;
         }
     }
