@@ -169,7 +169,7 @@ __device__ void write_bad_context(const FitArgs& a, const CtxDesc& ds) {
 // here), assigned to the kernel of their class, and each class list is sorted
 // by an estimate of the elimination work, largest first:
 //   class 0: fw <= 3, at most kLongRows rows  -> register basis, one wavefront
-//   class 1: fw 4-8, at most kLongRows rows   -> LDS basis, one wavefront
+//   class 1: fw 4-8, at most kLongRows rows   -> LDS basis, kPivWaves wavefronts
 //   class 2: fw <= 8, more than kLongRows rows -> LDS basis, kPivWaves wavefronts
 //   class 3: fw > 8                           -> large-context kernel
 // A class kernel with G workgroups deals its list out in stripes of G entries,
@@ -286,9 +286,10 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_scatter(FitArgs a, int bl
     }
 }
 
-// the i-th context of class cls dealt to this workgroup (snake order), or -1
-__device__ __forceinline__ int class_ctx(const FitArgs& a, int cls, int i) {
-    const int lo = a.plan[cls], cnt = a.plan[cls + 1] - lo;
+// the i-th context of classes cls .. cls_last (adjacent lists) dealt to this
+// workgroup (snake order), or -1
+__device__ __forceinline__ int class_ctx(const FitArgs& a, int cls, int i, int cls_last = -1) {
+    const int lo = a.plan[cls], cnt = a.plan[(cls_last < 0 ? cls : cls_last) + 1] - lo;
     const int G = static_cast<int>(gridDim.x), g = static_cast<int>(blockIdx.x);
     const int64_t e = static_cast<int64_t>(i) * G + ((i & 1) ? G - 1 - g : g);
     return e < cnt ? a.plan[kPlanHead + lo + static_cast<int>(e)] : -1;
@@ -619,9 +620,9 @@ __global__ __launch_bounds__(64 * kRegWaves) void k_fit_reg(FitArgs a) {
 
 // ---------------------------------------------------------------------------
 // pivot-indexed LDS-basis fit: retained row of pivot p in record p (fw + 2
-// words), a pivot-column bitmask beside it.  Used with one wavefront for short
-// contexts of 4-8 feature words and with NW wavefronts for long contexts of up
-// to 8 feature words.  With NW > 1 the next NW blocks of 64 rows are reduced
+// words), a pivot-column bitmask beside it, for contexts of 4-8 feature words
+// and for long contexts of up to 8 feature words.  With NW > 1 wavefronts (the
+// kernel runs kPivWaves) the next NW blocks of 64 rows are reduced
 // in parallel, one per wavefront; the first block (in stream order) that still
 // holds a nonzero feature residual runs the insertion loop in its own
 // wavefront, the blocks before it are only classified, the blocks after it are
@@ -889,23 +890,6 @@ __device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
         a.ctx_flags[c] = S.contra ? F2_CTX_CONTRADICTION : 0u;
     }
     __syncthreads();
-}
-
-// width class 1 (fw 4-8, short) with NW = 1; long contexts of fw <= 8 with NW = kPivWaves
-template <int NW>
-__global__ __launch_bounds__(64 * NW) void k_fit_piv(FitArgs a) {
-    __shared__ PivShared S;
-    for (int i = 0;; ++i) {
-        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsPiv, i));
-        if (c < 0) break;
-        const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
-        switch (feat_words(ds.n)) {
-            case 1: fit_ctx_piv<1, NW>(a, ds, S); break;
-            case 2: fit_ctx_piv<2, NW>(a, ds, S); break;
-            case 3: case 4: fit_ctx_piv<4, NW>(a, ds, S); break;
-            default: fit_ctx_piv<8, NW>(a, ds, S); break;
-        }
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1326,10 +1310,10 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
     }
 }
 
-// contexts of class 2 (fw <= 8, long: pivot-indexed LDS basis, kPivWaves wavefronts)
-// and class 3 (fw > 8: large-context path) share one launch: both run 8
-// wavefronts and are limited to one workgroup per compute unit, so the union of
-// their shared memory costs no occupancy
+// contexts of classes 1-2 (fw <= 8 beyond the register kernel: pivot-indexed LDS
+// basis, kPivWaves wavefronts) and class 3 (fw > 8: large-context path) share one
+// launch: both run 8 wavefronts and are limited to one workgroup per compute
+// unit, so the union of their shared memory costs no occupancy
 union WideShared {
     PivShared piv;
     LargeShared large;
@@ -1337,8 +1321,9 @@ union WideShared {
 
 __global__ __launch_bounds__(kLargeThreads) void k_fit_wide(FitArgs a) {
     __shared__ WideShared U;
+    // classes 1 and 2 are adjacent in the plan: one list of LDS-basis contexts
     for (int i = 0;; ++i) {
-        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsPivLong, i));
+        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsPiv, i, kClsPivLong));
         if (c < 0) break;
         const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
         switch (feat_words(ds.n)) {
@@ -1879,7 +1864,6 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
     hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
     hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid((C + kRegWaves - 1) / kRegWaves, 256)), dim3(64 * kRegWaves), 0, s, a);
-    hipLaunchKernelGGL(k_fit_piv<1>, dim3(fit_grid(C, 1024)), dim3(64), 0, s, a);
     hipLaunchKernelGGL(k_fit_wide, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
