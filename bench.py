@@ -47,6 +47,14 @@ WORKLOADS = {
                 "1% out of span"),
 }
 
+# streaming kernels outside the fit/encode step: (rows or words, k values per row, description)
+STREAM_WORKLOADS = {
+    "vectorize": (7_240_070, 5, "Eq. 1 rows from k=5 parsed 64-bit values (d=321) plus 128-bit outputs, "
+                                "7,240,070 rows (the row count of the n-in-[8,256] fit workload)"),
+    "merge": (100_000_000, 0, "100M encoded words: a 17-bit field XORed in at bit 105, opaque bits 122 and 124 "
+                              "restored from recorded state"),
+}
+
 
 def fit_bytes(wl, rank):
     """Algorithmic HBM bytes of one fit: rows, offsets and widths in; basis rows, pivots, maps and scalars out."""
@@ -138,12 +146,84 @@ def cpu_baseline(wl, ctx, x, stride, nq, do_fit):
     return out
 
 
+def bench_stream(args):
+    """Time the Eq. 1 row builder or the word merge alone on seeded data already in HBM."""
+    import numpy as np
+    import torch
+    from paper_2608_20532_amd import f2gpu
+    count, k, desc = STREAM_WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(0xF2A50010)
+    rnd = lambda n: torch.randint(-2 ** 63, 2 ** 63 - 1, (n,), generator=g, device=dev, dtype=torch.int64)
+    stream = torch.cuda.current_stream()
+    ALL = 2 ** 64 - 1
+    mask = (0, (1 << 58) | (1 << 60))
+    if args.workload == "vectorize":
+        vals, y = rnd(count * k), rnd(2 * count)
+        out = torch.empty(count * (k + 3), dtype=torch.int64, device=dev)
+        keep = (ALL, ALL & ~mask[1])
+        call = lambda: f2gpu.f2_vectorize_rows(vals, y, count, k, keep, out, stream.cuda_stream)
+        nbytes = count * (8 * k + 16 + 8 * (k + 3))
+        unit, kernel = "rows/s", "f2_vectorize_rows"
+    else:
+        words, field, state = rnd(2 * count), rnd(count) & ((1 << 17) - 1), rnd(2 * count)
+        out = torch.empty(2 * count, dtype=torch.int64, device=dev)
+        call = lambda: f2gpu.f2_merge_words(words, field, 105, 17, mask, state, count, out, stream.cuda_stream)
+        nbytes = count * (16 + 8 + 16 + 16)
+        unit, kernel = "words/s", "f2_merge_words"
+    for _ in range(args.warmup):
+        assert call() == 0
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    w0 = time.perf_counter()
+    for e in ev:
+        e[0].record(stream)
+        assert call() == 0
+        e[1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import words as W
+        rngc = np.random.default_rng(0)
+        t0, done = time.perf_counter(), 0
+        while time.perf_counter() - t0 < 10.0:
+            if args.workload == "vectorize":
+                v = rngc.integers(0, 2 ** 63, size=1000 * k, dtype=np.uint64)
+                yy = rngc.integers(0, 2 ** 63, size=2000, dtype=np.uint64)
+                W.vectorize_rows(v, k, yy, (ALL, ALL & ~mask[1]))
+                done += 1000
+            else:
+                ww = rngc.integers(0, 2 ** 63, size=20000, dtype=np.uint64)
+                ff = rngc.integers(0, 2 ** 17, size=10000, dtype=np.uint64)
+                W.merge_words(ww, ff, 105, 17, mask, rngc.integers(0, 2 ** 63, size=20000, dtype=np.uint64))
+                done += 10000
+        cpu = {"value": done / (time.perf_counter() - t0), "unit": unit, "cores": 1, "kind": "oracle",
+               "sample": f"oracle ({'rows' if k else 'words'} one at a time in Python integers) on {done} seeded "
+                         f"items of the same shape, about 10 s"}
+    print(json.dumps({
+        "metric": "GF(2) fit rows/sec and encoded words/sec on 1 MI355X; % of HBM/int-op roofline",
+        "value": count / (ms * 1e-3), "unit": unit, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": 1e3 * wall / args.steps, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u64", "data": "synthetic",
+        "config": {"workload": desc, "name": args.workload, "items": count},
+        "roofline": {"bound": "hbm", "kernel": kernel, "achieved": gbps, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbps / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes, "avg_ms": ms,
+                     "traffic_note": "no counters for this workload"},
+        "cpu_baseline": cpu,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="recipe2", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="recipe2", choices=sorted(WORKLOADS) + sorted(STREAM_WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (HBM counter calibration)")
@@ -166,6 +246,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 3}), flush=True)
+        return
+
+    if args.workload in STREAM_WORKLOADS:
+        bench_stream(args)
         return
 
     import synth

@@ -166,6 +166,42 @@ int f2_encode_batch(const f2_model* model_host, const int32_t* ctx_id, const uin
                     int64_t num_queries, uint64_t* words_out, uint8_t* qflags_out, void* workspace,
                     size_t workspace_bytes, void* stream);
 
+/*
+ * Feature vectors of Eq. 1 as fit rows.  Eq. 1 builds phi = [1 | bits64(v_0) |
+ * ... | bits64(v_{k-1})] from k parsed 64-bit values, d = 1 + 64k features;
+ * feature index 1 + 64j + b is bit b of v_j (the numbering of App. C).  In the
+ * row layout above (n = 64k) that is storage bit 64j + b, with the constant in
+ * word k, so row r becomes
+ *     [v_{r,0} .. v_{r,k-1} | 1 | y_r AND keep]         (k + 3 words)
+ *   values     [num_rows * k] row-major
+ *   y          [2 * num_rows] output words, or NULL for zero outputs
+ *   keep_host  [2] host words: output bits that are learned (all ones, or an
+ *              opaque mask cleared: those bits are restored after encoding by
+ *              f2_merge_words)
+ *   rows_out   [num_rows * (k + 3)]
+ * 0 <= k <= 63.  Queries need no conversion: x is the values, stride k words.
+ * Returns F2_OK, F2_EINVAL or F2_EDEVICE.
+ */
+int f2_vectorize_rows(const uint64_t* values, const uint64_t* y, int64_t num_rows, int32_t k,
+                      const uint64_t* keep_host, uint64_t* rows_out, void* stream);
+
+/*
+ * Final words from learned words (Sec. 4, the worked example that assembles an
+ * instruction word): a separately supplied field is shifted into place and
+ * XORed in, then the bits of an opaque mask (excluded from learning) are
+ * restored from recorded state.  For each q < num_words:
+ *     w = words[q] XOR ((field[q] AND (2^width - 1)) << shift)    (128-bit)
+ *     out[q] = (w AND NOT mask) OR (state[q] AND mask)
+ *   words, out [2 * num_words] (may be the same buffer)
+ *   field      [num_words], or NULL for no field (then width and shift are ignored)
+ *   width      1..64 bits, shift + width <= 128
+ *   mask_host  [2] host words; state [2 * num_words] or NULL (masked bits cleared)
+ * Returns F2_OK, F2_EINVAL or F2_EDEVICE.
+ */
+int f2_merge_words(const uint64_t* words, const uint64_t* field, int32_t shift, int32_t width,
+                   const uint64_t* mask_host, const uint64_t* state, int64_t num_words, uint64_t* out,
+                   void* stream);
+
 /* Static description of a status code. */
 const char* f2_status_string(int status);
 

@@ -1731,6 +1731,58 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_unsort(EncArgs e, SortArgs 
     e.qflags[q] = static_cast<uint8_t>(s.res[2 * i + 1].x);
 }
 
+// ---------------------------------------------------------------------------
+// feature vectors of Eq. 1 as fit rows, and the post-encode word merges: plain
+// streaming kernels, one output word (vectorize) or one 128-bit word (merge)
+// per thread, reads and writes coalesced
+// ---------------------------------------------------------------------------
+constexpr int kStreamThreads = 256;
+
+__global__ __launch_bounds__(kStreamThreads) void k_vectorize(const uint64_t* values, const uint64_t* y,
+                                                              int64_t num_rows, int k, uint64_t keep0,
+                                                              uint64_t keep1, uint64_t* rows) {
+    const int rw = k + 3;
+    const int64_t o = static_cast<int64_t>(blockIdx.x) * kStreamThreads + threadIdx.x;
+    if (o >= num_rows * rw) return;
+    const int64_t r = o / rw;
+    const int j = static_cast<int>(o - r * rw);
+    uint64_t v;
+    if (j < k) v = values[r * k + j];
+    else if (j == k) v = 1;  // the constant feature
+    else v = y ? (y[2 * r + (j - k - 1)] & (j == k + 1 ? keep0 : keep1)) : 0ull;
+    rows[o] = v;
+}
+
+__global__ __launch_bounds__(kStreamThreads) void k_merge(const uint64_t* words, const uint64_t* field, int shift,
+                                                          int width, uint64_t mask0, uint64_t mask1,
+                                                          const uint64_t* state, int64_t n, uint64_t* out) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kStreamThreads + threadIdx.x;
+    if (q >= n) return;
+    const Word2 w = *reinterpret_cast<const Word2*>(words + 2 * q);
+    uint64_t lo = w.x, hi = w.y;
+    if (field) {
+        const uint64_t f = width >= 64 ? field[q] : (field[q] & ((1ull << width) - 1));
+        if (shift == 0) {
+            lo ^= f;
+        } else if (shift < 64) {
+            lo ^= f << shift;
+            hi ^= f >> (64 - shift);
+        } else {
+            hi ^= f << (shift - 64);
+        }
+    }
+    uint64_t s0 = 0, s1 = 0;
+    if (state) {
+        const Word2 st = *reinterpret_cast<const Word2*>(state + 2 * q);
+        s0 = st.x;
+        s1 = st.y;
+    }
+    Word2 r;
+    r.x = (lo & ~mask0) | (s0 & mask0);
+    r.y = (hi & ~mask1) | (s1 & mask1);
+    *reinterpret_cast<Word2*>(out + 2 * q) = r;
+}
+
 inline size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
 // workgroups of a fit class kernel: at most one per context, at most `cap`
@@ -1925,6 +1977,34 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     hipLaunchKernelGGL(k_encode_sorted, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     if (!p.s.direct)
         hipLaunchKernelGGL(k_enc_unsort, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
+    return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
+}
+
+int f2_vectorize_rows(const uint64_t* values, const uint64_t* y, int64_t num_rows, int32_t k,
+                      const uint64_t* keep_host, uint64_t* rows_out, void* stream) {
+    if (num_rows < 0 || k < 0 || k > 63 || !keep_host) return F2_EINVAL;
+    if (num_rows == 0) return F2_OK;
+    if ((k > 0 && !values) || !rows_out) return F2_EINVAL;
+    const int64_t total = num_rows * (k + 3);
+    const int64_t blocks = (total + kStreamThreads - 1) / kStreamThreads;
+    if (num_rows > (int64_t{1} << 56) || blocks > 0x7fffffff) return F2_EINVAL;
+    hipLaunchKernelGGL(k_vectorize, dim3(static_cast<unsigned>(blocks)), dim3(kStreamThreads), 0,
+                       static_cast<hipStream_t>(stream), values, y, num_rows, k, keep_host[0], keep_host[1], rows_out);
+    return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
+}
+
+int f2_merge_words(const uint64_t* words, const uint64_t* field, int32_t shift, int32_t width,
+                   const uint64_t* mask_host, const uint64_t* state, int64_t num_words, uint64_t* out,
+                   void* stream) {
+    if (num_words < 0 || !mask_host) return F2_EINVAL;
+    if (field && (width < 1 || width > 64 || shift < 0 || shift + width > 128)) return F2_EINVAL;
+    if (num_words == 0) return F2_OK;
+    if (!words || !out) return F2_EINVAL;
+    const int64_t blocks = (num_words + kStreamThreads - 1) / kStreamThreads;
+    if (blocks > 0x7fffffff) return F2_EINVAL;
+    hipLaunchKernelGGL(k_merge, dim3(static_cast<unsigned>(blocks)), dim3(kStreamThreads), 0,
+                       static_cast<hipStream_t>(stream), words, field, field ? shift : 0, field ? width : 64,
+                       mask_host[0], mask_host[1], state, num_words, out);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 

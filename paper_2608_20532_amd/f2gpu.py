@@ -25,7 +25,7 @@ Q_OUT_OF_SPAN, Q_CTX_CONTRADICTORY, Q_BAD_CTX = 1, 2, 4
 
 # every entry point the header declares
 EXPORTS = ("f2_fit_layout", "f2_fit_workspace_bytes", "f2_fit_batch", "f2_encode_workspace_bytes",
-           "f2_encode_batch", "f2_status_string")
+           "f2_encode_batch", "f2_vectorize_rows", "f2_merge_words", "f2_status_string")
 
 
 class f2_model(ctypes.Structure):
@@ -65,6 +65,10 @@ def _load():
     L.f2_encode_workspace_bytes.restype = sz
     L.f2_encode_batch.argtypes = [MP, P, P, i32, i64, P, P, P, sz, P]
     L.f2_encode_batch.restype = ctypes.c_int
+    L.f2_vectorize_rows.argtypes = [P, P, i64, i32, P, P, P]
+    L.f2_vectorize_rows.restype = ctypes.c_int
+    L.f2_merge_words.argtypes = [P, P, i32, i32, P, P, i64, P, P]
+    L.f2_merge_words.restype = ctypes.c_int
     L.f2_status_string.argtypes = [ctypes.c_int]
     L.f2_status_string.restype = ctypes.c_char_p
     return L
@@ -160,6 +164,24 @@ def f2_encode_batch(model: Model, ctx_id, x, x_stride_words: int, num_queries: i
     return int(lib.f2_encode_batch(ctypes.byref(model.struct()), _ptr(ctx_id), _ptr(x), int(x_stride_words),
                                    int(num_queries), _ptr(words_out), _ptr(qflags_out), _ptr(workspace),
                                    int(workspace_bytes), _stream(stream)))
+
+
+def _host_words2(v) -> ctypes.Array:
+    a = (ctypes.c_uint64 * 2)()
+    a[0], a[1] = int(v[0]) & (2 ** 64 - 1), int(v[1]) & (2 ** 64 - 1)
+    return a
+
+
+def f2_vectorize_rows(values, y, num_rows: int, k: int, keep, rows_out, stream=None) -> int:
+    """Enqueue the Eq. 1 row builder; keep is a pair of host words; returns the status code."""
+    return int(lib.f2_vectorize_rows(_ptr(values), _ptr(y), int(num_rows), int(k), _host_words2(keep),
+                                     _ptr(rows_out), _stream(stream)))
+
+
+def f2_merge_words(words, field, shift: int, width: int, mask, state, num_words: int, out, stream=None) -> int:
+    """Enqueue the post-encode merge; mask is a pair of host words; returns the status code."""
+    return int(lib.f2_merge_words(_ptr(words), _ptr(field), int(shift), int(width), _host_words2(mask),
+                                  _ptr(state), int(num_words), _ptr(out), _stream(stream)))
 
 
 # ---- convenience wrappers used by tests and the benchmark (allocation + one call) ----

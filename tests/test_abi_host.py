@@ -78,3 +78,28 @@ def test_calls_with_bad_host_arguments_enqueue_nothing():
     assert L.f2_encode_batch(ctypes.byref(m), None, None, 1, 0, None, None, None, 0, None) == f2gpu.F2_OK
     m.num_ctx = 3
     assert L.f2_fit_batch(None, 0, None, ctypes.byref(m), None, 0, None) == f2gpu.F2_EINVAL
+
+
+def test_vectorize_and_merge_argument_errors():
+    """The row builder and the word merge reject bad sizes before any device work."""
+    from paper_2608_20532_amd import f2gpu
+    keep = (2 ** 64 - 1, 2 ** 64 - 1)
+    V = f2gpu.f2_vectorize_rows
+    assert V(None, None, 10, 64, keep, None, 0) == f2gpu.F2_EINVAL       # k above 63
+    assert V(None, None, 10, -1, keep, None, 0) == f2gpu.F2_EINVAL
+    assert V(None, None, -1, 2, keep, None, 0) == f2gpu.F2_EINVAL
+    assert V(None, None, 0, 2, keep, None, 0) == f2gpu.F2_OK              # nothing to do
+    assert V(None, None, 5, 2, keep, None, 0) == f2gpu.F2_EINVAL          # values and output missing
+    assert f2gpu.lib.f2_vectorize_rows(None, None, 5, 0, None, None, None) == f2gpu.F2_EINVAL  # no keep mask
+    M = f2gpu.f2_merge_words
+
+    class Fake:  # a non-null device pointer stand-in: the call must fail before using it
+        def data_ptr(self):
+            return 256
+    f = Fake()
+    for shift, width in ((0, 0), (0, 65), (-1, 5), (100, 29), (64, 65)):
+        assert M(f, f, shift, width, (0, 0), None, 8, f, 0) == f2gpu.F2_EINVAL, (shift, width)
+    assert M(None, None, 0, 0, (0, 0), None, 0, None, 0) == f2gpu.F2_OK
+    assert M(None, None, 0, 0, (0, 0), None, 3, None, 0) == f2gpu.F2_EINVAL
+    assert M(f, None, 0, 0, (0, 0), None, -2, f, 0) == f2gpu.F2_EINVAL
+    assert f2gpu.lib.f2_merge_words(None, None, 0, 0, None, None, 0, None, None) == f2gpu.F2_EINVAL
