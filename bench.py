@@ -53,6 +53,8 @@ STREAM_WORKLOADS = {
                                 "7,240,070 rows (the row count of the n-in-[8,256] fit workload)"),
     "merge": (100_000_000, 0, "100M encoded words: a 17-bit field XORed in at bit 105, opaque bits 122 and 124 "
                               "restored from recorded state"),
+    "pool": (80_000, 3, "pool the bases of 240,000 shard contexts (each n-in-[8,256] context's rows split in 3, "
+                        "fitted apart) back into 80,000 contexts"),
 }
 
 
@@ -218,6 +220,84 @@ def bench_stream(args):
     }), flush=True)
 
 
+def bench_pool(args):
+    """Time f2_pool_bases: shard bases of every context pooled back into one context each."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2608_20532_amd import f2gpu
+    C0, parts, desc = STREAM_WORKLOADS["pool"]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(0)
+    wl0 = synth.fit_workload(3, num_ctx=C0)
+    n_bits, rows_list = [], []
+    for c in range(C0):
+        n = int(wl0.n_bits[c])
+        W = (n + 64) // 64 + 2
+        for part in np.array_split(wl0.rows[wl0.row_off[c]:wl0.row_off[c + 1]].reshape(-1, W), parts):
+            n_bits.append(n)
+            rows_list.append(part)
+    wl = synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+    to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int64) if a.dtype == np.uint64 else a).to(dev)
+    members_model = f2gpu.fit(to_dev(wl.rows), to_dev(wl.row_off), wl.n_bits)
+    pool_off = to_dev(np.arange(0, parts * C0 + 1, parts, dtype=np.int64))
+    members = to_dev(np.arange(parts * C0, dtype=np.int32))
+    pooled = f2gpu.Model(wl0.n_bits, device=dev)
+    flags = torch.zeros(C0, dtype=torch.int32, device=dev)
+    nb = f2gpu.f2_pool_workspace_bytes(members_model, C0)
+    ws = f2gpu.workspace(nb, dev)
+    stream = torch.cuda.current_stream()
+    call = lambda: f2gpu.f2_pool_bases(members_model, None, pool_off, members, parts * C0, pooled, flags, ws, nb,
+                                       stream.cuda_stream)
+    for _ in range(args.warmup):
+        assert call() == 0
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    w0 = time.perf_counter()
+    for e in ev:
+        e[0].record(stream)
+        assert call() == 0
+        e[1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    mrank = members_model.rank.cpu().numpy()[:parts * C0].astype(np.int64)
+    prank = pooled.rank.cpu().numpy()[:C0].astype(np.int64)
+    Wm = (np.asarray(n_bits, np.int64) + 64) // 64 + 2
+    Wp = (wl0.n_bits.astype(np.int64) + 64) // 64 + 2
+    rows_in = int(mrank.sum())
+    nbytes = int((mrank * Wm * 8).sum() + (prank * Wp * 8).sum() + 4 * prank.sum() +
+                 (16 * (wl0.n_bits.astype(np.int64) + 1)).sum() + 20 * C0 + 4 * parts * C0 + 8 * (C0 + 1))
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    shared = int((flags.cpu().numpy()[:C0] == f2gpu.POOL_SHARED).sum())
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import pool as PL
+        ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+        t0, done, k = time.perf_counter(), 0, 0
+        while time.perf_counter() - t0 < 10.0 and k < C0:
+            k1 = min(C0, k + 2000)
+            mem = np.arange(parts * k, parts * k1)
+            PL.pool_bases(ref, np.concatenate([[0], np.cumsum(np.full(k1 - k, parts))]), mem, wl0.n_bits[k:k1])
+            done += int(mrank[parts * k:parts * k1].sum())
+            k = k1
+        cpu = {"value": done / (time.perf_counter() - t0), "unit": "basis rows/s", "cores": 1, "kind": "oracle",
+               "sample": f"oracle pooling of the first {k} pools ({done} member basis rows), about 10 s"}
+    print(json.dumps({
+        "metric": "GF(2) fit rows/sec and encoded words/sec on 1 MI355X; % of HBM/int-op roofline",
+        "value": rows_in / (ms * 1e-3), "unit": "basis rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": 1e3 * wall / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": desc, "name": "pool", "pools": C0, "member_contexts": parts * C0,
+                   "member_basis_rows": rows_in, "shared_pools": shared},
+        "roofline": {"bound": "hbm", "kernel": "f2_pool_bases", "achieved": gbps, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": gbps / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes,
+                     "avg_ms": ms, "traffic_note": "no counters for this workload"},
+        "cpu_baseline": cpu,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -248,6 +328,9 @@ def main():
         print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 3}), flush=True)
         return
 
+    if args.workload == "pool":
+        bench_pool(args)
+        return
     if args.workload in STREAM_WORKLOADS:
         bench_stream(args)
         return

@@ -202,6 +202,40 @@ int f2_merge_words(const uint64_t* words, const uint64_t* field, int32_t shift, 
                    const uint64_t* mask_host, const uint64_t* state, int64_t num_words, uint64_t* out,
                    void* stream);
 
+/* per-pool flags (pool_flags) */
+enum {
+    F2_POOL_SHARED = 1u,          /* one map serves every member */
+    F2_POOL_CONTRADICTION = 2u,   /* the members' equations contradict each other */
+    F2_POOL_WIDTH_MISMATCH = 4u,  /* a member's width differs from the pool's (pool fitted from no rows) */
+    F2_POOL_MASK_MISMATCH = 8u,   /* the members' output masks differ */
+    F2_POOL_BAD_MEMBER = 16u      /* a member id out of range, a malformed or contradictory member, bad
+                                     pool offsets, or members used by several pools beyond the buffer
+                                     (pool fitted from no rows) */
+};
+
+/*
+ * Pooling of separately fitted contexts (Sec. 2.1: groups with the same
+ * instruction form are trained apart, then their bases are combined and
+ * eliminated; one shared map is kept when the equations are consistent and the
+ * output masks match, otherwise the maps stay separate; Sec. 2.2 merges shard
+ * bases the same way).  Pool p has the member contexts
+ * members[pool_off[p] .. pool_off[p+1]) of members_model; their basis rows, in
+ * member order and each member's stored order, are fitted as one row stream
+ * (f2_fit_batch semantics) into context p of pooled.
+ *   out_mask   [2 * members_model->num_ctx] learned-bit mask per member context,
+ *              or NULL (all equal)
+ *   pooled     outputs; pooled->num_ctx pools, pooled->n_bits[p] the pool's width
+ *   pool_flags [pooled->num_ctx] F2_POOL_* flags: SHARED alone, or the reasons
+ * Each context should appear in at most one pool (the row buffer holds every
+ * member basis once).  For consistent members the pooled basis is the fully
+ * reduced basis of the union of their spans.
+ * Returns F2_OK, F2_EINVAL, F2_EWORKSPACE or F2_EDEVICE.
+ */
+size_t f2_pool_workspace_bytes(const f2_model* members_model, int32_t num_pools);
+int f2_pool_bases(const f2_model* members_model, const uint64_t* out_mask, const int64_t* pool_off,
+                  const int32_t* members, int64_t num_members, const f2_model* pooled, uint32_t* pool_flags,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* f2_status_string(int status);
 

@@ -1783,6 +1783,124 @@ __global__ __launch_bounds__(kStreamThreads) void k_merge(const uint64_t* words,
     *reinterpret_cast<Word2*>(out + 2 * q) = r;
 }
 
+// ---------------------------------------------------------------------------
+// basis pooling: contexts trained separately (one per exact group) are tested
+// for one shared map by eliminating their bases together.  The members' basis
+// rows are concatenated per pool (count -> scan -> copy) and fitted by the fit
+// kernels as ordinary row streams; a pool is shared when that fit finds no
+// contradiction and its members are valid, consistent and of equal width and
+// output mask.
+// ---------------------------------------------------------------------------
+struct PoolArgs {
+    int32_t num_ctx;  // members' model
+    const int32_t* n_bits;
+    const int64_t* basis_off;
+    const uint64_t* basis;
+    const int32_t* rank;
+    const uint32_t* ctx_flags;
+    const uint64_t* out_mask;  // [2 num_ctx] or null
+    int32_t num_pools;
+    const int64_t* pool_off;   // [num_pools + 1] into members
+    const int32_t* members;
+    int64_t num_members;
+    const int32_t* pooled_n;   // widths of the pooled contexts
+    const uint32_t* pooled_flags;
+    uint32_t* pool_flags;
+    int64_t* row_off;          // [num_pools + 1]: row words per pool, then their offsets
+    uint64_t* rows;
+    int64_t rows_cap;
+};
+
+constexpr uint32_t kPoolNoRows = F2_POOL_BAD_MEMBER | F2_POOL_WIDTH_MISMATCH;
+
+__global__ __launch_bounds__(256) void k_pool_count(PoolArgs P) {
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p >= P.num_pools) return;
+    const int64_t lo = P.pool_off[p], hi = P.pool_off[p + 1];
+    const int n = P.pooled_n[p];
+    const int64_t W = feat_words(n < 0 ? 0 : n) + F2_Y_WORDS;
+    uint32_t fl = (lo < 0 || hi < lo || hi > P.num_members || n < 0 || n > F2_MAX_N_BITS) ? F2_POOL_BAD_MEMBER : 0u;
+    int64_t words = 0;
+    uint64_t m0 = 0, m1 = 0;
+    for (int64_t e = lo; e < hi && !(fl & F2_POOL_BAD_MEMBER); ++e) {
+        const int c = P.members[e];
+        if (c < 0 || c >= P.num_ctx || P.ctx_flags[c] != 0) {  // out of range, malformed or contradictory
+            fl |= F2_POOL_BAD_MEMBER;
+            break;
+        }
+        if (P.n_bits[c] != n) fl |= F2_POOL_WIDTH_MISMATCH;
+        if (P.out_mask) {
+            const uint64_t a0 = P.out_mask[2 * c], a1 = P.out_mask[2 * c + 1];
+            if (e == lo) {
+                m0 = a0;
+                m1 = a1;
+            } else if (a0 != m0 || a1 != m1) {
+                fl |= F2_POOL_MASK_MISMATCH;
+            }
+        }
+        words += static_cast<int64_t>(P.rank[c]) * W;
+    }
+    P.pool_flags[p] = fl;
+    P.row_off[p] = (fl & kPoolNoRows) ? 0 : words;
+}
+
+// one workgroup: exclusive scan of the row words; a total beyond the buffer (a
+// context in several pools) empties every pool and flags it
+__global__ __launch_bounds__(1024) void k_pool_scan(PoolArgs P) {
+    __shared__ int64_t sWave[16];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int per = (P.num_pools + 1023) / 1024;
+    const int p0 = tid * per;
+    int64_t sum = 0;
+    for (int k = 0; k < per; ++k)
+        if (p0 + k < P.num_pools) sum += P.row_off[p0 + k];
+    int64_t x = sum;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int64_t t = __shfl_up(x, o);
+        if (lane >= o) x += t;
+    }
+    if (lane == 63) sWave[tid >> 6] = x;
+    __syncthreads();
+    int64_t run = x - sum, total = 0;
+    for (int w = 0; w < 16; ++w) {
+        total += sWave[w];
+        if (w < (tid >> 6)) run += sWave[w];
+    }
+    const bool over = total > P.rows_cap;
+    for (int k = 0; k < per; ++k)
+        if (p0 + k < P.num_pools) {
+            const int64_t v = P.row_off[p0 + k];
+            P.row_off[p0 + k] = over ? 0 : run;
+            if (over) P.pool_flags[p0 + k] |= F2_POOL_BAD_MEMBER;
+            run += v;
+        }
+    if (tid == 0) P.row_off[P.num_pools] = over ? 0 : total;
+}
+
+// one workgroup per pool: the members' basis rows, in member order, each in its stored order
+__global__ __launch_bounds__(256) void k_pool_copy(PoolArgs P) {
+    const int p = blockIdx.x;
+    if (P.pool_flags[p] & kPoolNoRows) return;
+    const int64_t lo = P.pool_off[p], hi = P.pool_off[p + 1];
+    const int64_t W = feat_words(P.pooled_n[p]) + F2_Y_WORDS;
+    int64_t dst = P.row_off[p];
+    for (int64_t e = lo; e < hi; ++e) {
+        const int c = P.members[e];
+        const int64_t words = static_cast<int64_t>(P.rank[c]) * W;
+        const uint64_t* src = P.basis + P.basis_off[c];
+        for (int64_t k = threadIdx.x; k < words; k += 256) P.rows[dst + k] = src[k];
+        dst += words;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_pool_finish(PoolArgs P) {
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p >= P.num_pools) return;
+    uint32_t fl = P.pool_flags[p];
+    if (P.pooled_flags[p] & F2_CTX_CONTRADICTION) fl |= F2_POOL_CONTRADICTION;
+    P.pool_flags[p] = fl ? fl : F2_POOL_SHARED;
+}
+
 inline size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
 // workgroups of a fit class kernel: at most one per context, at most `cap`
@@ -1831,6 +1949,49 @@ EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     }
     p.bytes = o > 256 ? o : 256;
     return p;
+}
+
+// every output buffer of a model present and its sizes non-negative
+bool model_complete(const f2_model* m) {
+    return m->n_bits && m->basis_off && m->piv_off && m->map_off && m->basis && m->pivots && m->maps && m->tables &&
+           m->rank && m->ctx_flags && m->n_contra && m->first_contra_row && m->basis_words >= 0 &&
+           m->piv_entries >= 0 && m->map_words >= 0;
+}
+
+FitArgs fit_args(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m, int32_t* plan) {
+    FitArgs a;
+    a.rows = rows;
+    a.rows_words = rows_words;
+    a.row_off = row_off;
+    a.num_ctx = m->num_ctx;
+    a.n_bits = m->n_bits;
+    a.basis_off = m->basis_off;
+    a.piv_off = m->piv_off;
+    a.map_off = m->map_off;
+    a.basis_words = m->basis_words;
+    a.piv_entries = m->piv_entries;
+    a.map_words = m->map_words;
+    a.basis = m->basis;
+    a.pivots = m->pivots;
+    a.maps = m->maps;
+    a.tables = m->tables;
+    a.rank = m->rank;
+    a.ctx_flags = m->ctx_flags;
+    a.n_contra = m->n_contra;
+    a.first_contra = m->first_contra_row;
+    a.plan = plan;
+    return a;
+}
+
+// the fit: plan (two kernels), then the class kernels, each keeping about as
+// many workgroups as fit on the chip at once
+void launch_fit(const FitArgs& a, hipStream_t s) {
+    const int32_t C = a.num_ctx;
+    const int plan_blocks = static_cast<int>((static_cast<int64_t>(C) + kPlanThreads - 1) / kPlanThreads);
+    hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
+    hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
+    hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid((C + kRegWaves - 1) / kRegWaves, 256)), dim3(64 * kRegWaves), 0, s, a);
+    hipLaunchKernelGGL(k_fit_wide, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
 }
 
 }  // namespace
@@ -1882,41 +2043,11 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     if (!m || m->num_ctx < 0 || rows_words < 0) return F2_EINVAL;
     const int32_t C = m->num_ctx;
     if (C == 0) return F2_OK;
-    if (!row_off || !m->n_bits || !m->basis_off || !m->piv_off || !m->map_off || !m->basis || !m->pivots ||
-        !m->maps || !m->tables || !m->rank || !m->ctx_flags || !m->n_contra || !m->first_contra_row || (rows_words > 0 && !rows) ||
-        m->basis_words < 0 || m->piv_entries < 0 || m->map_words < 0)
-        return F2_EINVAL;
+    if (!row_off || !model_complete(m) || (rows_words > 0 && !rows)) return F2_EINVAL;
     if (!workspace || workspace_bytes < f2_fit_workspace_bytes(C) ||
         (reinterpret_cast<uintptr_t>(workspace) & 255u))
         return F2_EWORKSPACE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    FitArgs a;
-    a.rows = rows;
-    a.rows_words = rows_words;
-    a.row_off = row_off;
-    a.num_ctx = C;
-    a.n_bits = m->n_bits;
-    a.basis_off = m->basis_off;
-    a.piv_off = m->piv_off;
-    a.map_off = m->map_off;
-    a.basis_words = m->basis_words;
-    a.piv_entries = m->piv_entries;
-    a.map_words = m->map_words;
-    a.basis = m->basis;
-    a.pivots = m->pivots;
-    a.maps = m->maps;
-    a.tables = m->tables;
-    a.rank = m->rank;
-    a.ctx_flags = m->ctx_flags;
-    a.n_contra = m->n_contra;
-    a.first_contra = m->first_contra_row;
-    a.plan = static_cast<int32_t*>(workspace);
-    // each class kernel keeps about as many workgroups as fit on the chip at once
-    const int plan_blocks = static_cast<int>((static_cast<int64_t>(C) + kPlanThreads - 1) / kPlanThreads);
-    hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
-    hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
-    hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid((C + kRegWaves - 1) / kRegWaves, 256)), dim3(64 * kRegWaves), 0, s, a);
-    hipLaunchKernelGGL(k_fit_wide, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
+    launch_fit(fit_args(rows, rows_words, row_off, m, static_cast<int32_t*>(workspace)), static_cast<hipStream_t>(stream));
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 
@@ -2005,6 +2136,58 @@ int f2_merge_words(const uint64_t* words, const uint64_t* field, int32_t shift, 
     hipLaunchKernelGGL(k_merge, dim3(static_cast<unsigned>(blocks)), dim3(kStreamThreads), 0,
                        static_cast<hipStream_t>(stream), words, field, field ? shift : 0, field ? width : 64,
                        mask_host[0], mask_host[1], state, num_words, out);
+    return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
+}
+
+size_t f2_pool_workspace_bytes(const f2_model* members_model, int32_t num_pools) {
+    if (!members_model || members_model->basis_words < 0 || num_pools < 0) return 0;
+    return align256(sizeof(int64_t) * (static_cast<size_t>(num_pools) + 1)) +
+           align256(sizeof(uint64_t) * static_cast<size_t>(members_model->basis_words)) +
+           f2_fit_workspace_bytes(num_pools);
+}
+
+int f2_pool_bases(const f2_model* members_model, const uint64_t* out_mask, const int64_t* pool_off,
+                  const int32_t* members, int64_t num_members, const f2_model* pooled, uint32_t* pool_flags,
+                  void* workspace, size_t workspace_bytes, void* stream) {
+    if (!members_model || !pooled || members_model->num_ctx < 0 || pooled->num_ctx < 0 || num_members < 0)
+        return F2_EINVAL;
+    const int32_t P = pooled->num_ctx;
+    if (P == 0) return F2_OK;
+    if (!pool_off || !pool_flags || (num_members > 0 && !members) || !model_complete(pooled)) return F2_EINVAL;
+    if (members_model->num_ctx > 0 && (!members_model->n_bits || !members_model->basis_off || !members_model->basis ||
+                                       !members_model->rank || !members_model->ctx_flags || members_model->basis_words < 0))
+        return F2_EINVAL;
+    if (!workspace || workspace_bytes < f2_pool_workspace_bytes(members_model, P) ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u))
+        return F2_EWORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char* ws = static_cast<char*>(workspace);
+    PoolArgs A;
+    A.num_ctx = members_model->num_ctx;
+    A.n_bits = members_model->n_bits;
+    A.basis_off = members_model->basis_off;
+    A.basis = members_model->basis;
+    A.rank = members_model->rank;
+    A.ctx_flags = members_model->ctx_flags;
+    A.out_mask = out_mask;
+    A.num_pools = P;
+    A.pool_off = pool_off;
+    A.members = members;
+    A.num_members = num_members;
+    A.pooled_n = pooled->n_bits;
+    A.pooled_flags = pooled->ctx_flags;
+    A.pool_flags = pool_flags;
+    A.row_off = reinterpret_cast<int64_t*>(ws);
+    const size_t off_rows = align256(sizeof(int64_t) * (static_cast<size_t>(P) + 1));
+    A.rows = reinterpret_cast<uint64_t*>(ws + off_rows);
+    A.rows_cap = members_model->basis_words;
+    int32_t* plan = reinterpret_cast<int32_t*>(ws + off_rows + align256(sizeof(uint64_t) * A.rows_cap));
+    const unsigned pb = static_cast<unsigned>((P + 255) / 256);
+    hipLaunchKernelGGL(k_pool_count, dim3(pb), dim3(256), 0, s, A);
+    hipLaunchKernelGGL(k_pool_scan, dim3(1), dim3(1024), 0, s, A);
+    hipLaunchKernelGGL(k_pool_copy, dim3(static_cast<unsigned>(P)), dim3(256), 0, s, A);
+    launch_fit(fit_args(A.rows, A.rows_cap, A.row_off, pooled, plan), s);
+    hipLaunchKernelGGL(k_pool_finish, dim3(pb), dim3(256), 0, s, A);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 

@@ -22,10 +22,12 @@ F2_OK, F2_EINVAL, F2_EWORKSPACE, F2_EDEVICE, F2_ETOOWIDE = 0, -1, -2, -3, -4
 F2_MAX_N_BITS = 4095
 CTX_CONTRADICTION, CTX_BAD_SEGMENT, CTX_BAD_WIDTH, CTX_BAD_OUTPUT = 1, 2, 4, 8
 Q_OUT_OF_SPAN, Q_CTX_CONTRADICTORY, Q_BAD_CTX = 1, 2, 4
+POOL_SHARED, POOL_CONTRADICTION, POOL_WIDTH_MISMATCH, POOL_MASK_MISMATCH, POOL_BAD_MEMBER = 1, 2, 4, 8, 16
 
 # every entry point the header declares
 EXPORTS = ("f2_fit_layout", "f2_fit_workspace_bytes", "f2_fit_batch", "f2_encode_workspace_bytes",
-           "f2_encode_batch", "f2_vectorize_rows", "f2_merge_words", "f2_status_string")
+           "f2_encode_batch", "f2_vectorize_rows", "f2_merge_words", "f2_pool_workspace_bytes", "f2_pool_bases",
+           "f2_status_string")
 
 
 class f2_model(ctypes.Structure):
@@ -69,6 +71,10 @@ def _load():
     L.f2_vectorize_rows.restype = ctypes.c_int
     L.f2_merge_words.argtypes = [P, P, i32, i32, P, P, i64, P, P]
     L.f2_merge_words.restype = ctypes.c_int
+    L.f2_pool_workspace_bytes.argtypes = [MP, i32]
+    L.f2_pool_workspace_bytes.restype = sz
+    L.f2_pool_bases.argtypes = [MP, P, P, P, i64, MP, P, P, sz, P]
+    L.f2_pool_bases.restype = ctypes.c_int
     L.f2_status_string.argtypes = [ctypes.c_int]
     L.f2_status_string.restype = ctypes.c_char_p
     return L
@@ -184,6 +190,18 @@ def f2_merge_words(words, field, shift: int, width: int, mask, state, num_words:
                                   _ptr(state), int(num_words), _ptr(out), _stream(stream)))
 
 
+def f2_pool_workspace_bytes(members_model: "Model", num_pools: int) -> int:
+    return int(lib.f2_pool_workspace_bytes(ctypes.byref(members_model.struct()), int(num_pools)))
+
+
+def f2_pool_bases(members_model: "Model", out_mask, pool_off, members, num_members: int, pooled: "Model", pool_flags,
+                  workspace, workspace_bytes: int, stream=None) -> int:
+    """Enqueue the pooling of member bases into the pooled model; returns the status code."""
+    return int(lib.f2_pool_bases(ctypes.byref(members_model.struct()), _ptr(out_mask), _ptr(pool_off), _ptr(members),
+                                 int(num_members), ctypes.byref(pooled.struct()), _ptr(pool_flags), _ptr(workspace),
+                                 int(workspace_bytes), _stream(stream)))
+
+
 # ---- convenience wrappers used by tests and the benchmark (allocation + one call) ----
 
 def workspace(nbytes: int, device="cuda"):
@@ -199,6 +217,21 @@ def fit(rows_dev, row_off_dev, n_bits_host, stream=None):
     _check(f2_fit_batch(rows_dev, rows_dev.numel(), row_off_dev, model, ws, nb, stream), "f2_fit_batch")
     model._fit_ws = ws
     return model
+
+
+def pool(members_model: Model, pool_off_dev, members_dev, pooled_n_host, out_mask_dev=None, stream=None):
+    """Pool member bases; returns (pooled Model, pool_flags uint32-as-int32 device tensor)."""
+    import torch
+    dev = members_model.basis.device
+    pooled = Model(pooled_n_host, device=dev)
+    P = pooled.num_ctx
+    flags = torch.zeros(max(P, 1), dtype=torch.int32, device=dev)
+    nb = f2_pool_workspace_bytes(members_model, P)
+    ws = workspace(nb, dev)
+    _check(f2_pool_bases(members_model, out_mask_dev, pool_off_dev, members_dev, int(members_dev.numel()), pooled,
+                         flags, ws, nb, stream), "f2_pool_bases")
+    pooled._pool_ws = ws
+    return pooled, flags
 
 
 def encode(model: Model, ctx_dev, x_dev, stride: int, stream=None):
