@@ -35,7 +35,6 @@ namespace {
 
 constexpr int kLargeRows = 64;       // rows per block, large path
 constexpr int kLargeThreads = 512;
-constexpr int kMaxW = 66;            // widest row: 64 feature words + 2 output words
 constexpr int kEncThreads = 256;
 
 struct FitArgs {
@@ -893,17 +892,28 @@ __device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
 }
 
 // ---------------------------------------------------------------------------
-// large-context fit (fw > 8): one workgroup of 8 wavefronts per context, the
-// lanes of a wavefront spanning the words of a row.  The working basis lives in
-// the caller's basis buffer, one slot per priority position (slot t holds the
-// row whose pivot is the t-th highest-priority feature), so that the final
-// descending-priority order is an in-place compaction.  Rows go in blocks of 64:
-//   (1) block reduce: each wavefront reduces 8 rows of the block against every
-//       retained row; the selection bits are the rows' unreduced bits at the
-//       pivot columns (the basis is fully reduced), read a pivot word at a time;
-//   (2) in-block elimination in stream order;
-//   (3) the block's new rows are fully reduced among themselves;
-//   (4) the new pivots are cleared from the retained rows; (5) insertion.
+// large-context fit (fw > 8): one workgroup of 8 wavefronts per context.  Lanes
+// span the feature words of a row (lane w holds word w); the two output words of
+// the 8 rows a wavefront holds sit in lanes 2k, 2k+1 of one more register.  The
+// working basis lives in the caller's basis buffer, one slot per priority
+// position (slot t holds the row whose pivot is the t-th highest-priority
+// feature), and is kept fully reduced, so the final descending-priority order is
+// an in-place compaction.  Rows go in blocks of 64, row i of a block held by
+// wavefront i mod 8:
+//   (1) block reduce with Four-Russians tables (the method of Arlazarov, Dinic,
+//       Kronrod and Faradzev): the retained rows of four consecutive pivot
+//       positions give a 16-entry LDS table of all their XOR combinations, and a
+//       row's own four bits at those positions (unchanged by the other retained
+//       rows, the basis being fully reduced) select the entry to add.  Eight
+//       tables (32 pivot positions) are built per round while the previous
+//       round's tables are read;
+//   (2) in-block elimination in stream order with one workgroup barrier per row:
+//       the wavefront holding the row finds its pivot and publishes the row, and
+//       every wavefront clears that pivot from the other rows it holds (earlier
+//       new rows included, so the block's new rows end fully reduced);
+//   (3) back-substitution: the new rows, in descending priority, form tables of
+//       four rows each, and every retained row adds the entry its bits at those
+//       pivots select; (4) the new rows are stored at their priority slots.
 // Once the rank reaches d every later row lies in the span and the basis is the
 // identity on the features, so a row's residual is y + M phi (the canonical
 // map, staged in LDS): those rows are only checked for contradictions.
@@ -911,403 +921,481 @@ __device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
 __device__ __forceinline__ int prio_slot(int p, int n) { return p < n ? n - 1 - p : n; }
 __device__ __forceinline__ int slot_pivot(int t, int n) { return t < n ? n - 1 - t : n; }
 
-constexpr int kLargeWaves = kLargeThreads / 64;
-constexpr int kRowsPerWave = kLargeRows / kLargeWaves;
-
-// Stage the retained rows whose pivots are the set bits of pivot word pw into
-// dst[0 .. popc): wavefront v copies the rows of bits v, v+8, ... (lanes over
-// words); a row's staging index is the number of set bits below its bit.
-__device__ __forceinline__ void stage_rows(uint64_t (*dst)[kMaxW], const uint64_t* B, uint64_t pmw, int pw, int n,
-                                           int W, int wave, int lane) {
-    for (int b = wave; b < 64; b += kLargeWaves) {
-        if (!((pmw >> b) & 1ull)) continue;
-        const int r = __popcll(pmw & ((1ull << b) - 1));
-        const uint64_t* src = B + static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W;
-        if (lane < W) dst[r][lane] = src[lane];
-        if (64 + lane < W) dst[r][64 + lane] = src[64 + lane];
-    }
-}
-
-__device__ __forceinline__ void unstage_rows(const uint64_t (*src)[kMaxW], uint64_t* B, uint64_t pmw, int pw, int n,
-                                             int W, int wave, int lane) {
-    for (int b = wave; b < 64; b += kLargeWaves) {
-        if (!((pmw >> b) & 1ull)) continue;
-        const int r = __popcll(pmw & ((1ull << b) - 1));
-        uint64_t* dst = B + static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W;
-        if (lane < W) dst[lane] = src[r][lane];
-        if (64 + lane < W) dst[64 + lane] = src[r][64 + lane];
-    }
-}
+constexpr int kLargeWaves = kLargeThreads / 64;      // 8
+constexpr int kLgSlots = kLargeRows / kLargeWaves;   // block rows per wavefront: 8
+constexpr int kLgEnt = 16;                           // entries of a 4-bit table
+constexpr int kLgRoundTables = kLargeWaves;          // reduce: one table per wavefront per round
+constexpr int kLgBuf = kLgRoundTables * kLgEnt;      // entries of one round's tables
+static_assert(kLgSlots == 8, "a wavefront's output words occupy lanes 0-15");
+static_assert(kLgRoundTables * 4 == 32, "a round covers half a pivot word");
 
 struct LargeShared {
-    uint64_t sRow[kLargeRows][kMaxW];
-    // one buffer, two uses: two halves of staged retained rows (blocked phase), map columns (full-rank phase)
-    uint64_t sBuf[2 * kLargeRows * kMaxW];
-    uint64_t sPmask[64];
-    uint64_t sNew[kLargeRows][kMaxW];  // the block's new rows, in insertion order
-    int sNewRow[kLargeRows];           // block row of the k-th new pivot
-    int sNewPiv[kLargeRows];           // its pivot
-    int sNumNew, sContra;
-    long long sFirst, sFirstCons;
+    uint64_t tf[2 * kLgBuf][64];  // table entries, feature words (lane = word); the map in the full-rank phase
+    uint64_t tz[2 * kLgBuf][2];   // table entries, output words
+    uint64_t pivF[2][64];         // in-block elimination: the published row
+    uint64_t pivZ[2][2];
+    int pivP[2];
+    int rowPiv[kLargeRows];       // pivot of each block row that became a basis row, else -1
+    int nsorted[kLargeRows];      // the block's new pivots in descending priority
+    int above[64];                // new pivots (constant excluded) in feature words above w
+    uint64_t pm[64];              // pivot columns of the retained basis
+    uint64_t npm[64];             // pivot columns found in the current block
+    unsigned long long live;      // block rows with a nonzero feature residual after the reduce
+    int contra, nnew;
+    long long firstMin;
 };
 
-__device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& ds, LargeShared& L) {
-    uint64_t (&sRow)[kLargeRows][kMaxW] = L.sRow;
-    uint64_t* sBuf = L.sBuf;
-    uint64_t (*sZ)[2] = reinterpret_cast<uint64_t (*)[2]>(L.sBuf);
-    uint64_t* sPmask = L.sPmask;
-    uint64_t (&sNew)[kLargeRows][kMaxW] = L.sNew;
-    int* sNewRow = L.sNewRow;
-    int* sNewPiv = L.sNewPiv;
-    int& sNumNew = L.sNumNew;
-    int& sContra = L.sContra;
-    long long& sFirst = L.sFirst;
-    long long& sFirstCons = L.sFirstCons;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    {
-      {
-        const int c = ds.c;
-        const int n = ds.n;
-        const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
-        const int64_t m = ds.m;
-        const uint64_t* R = a.rows + ds.row0;
-        const uint64_t tmask = top_mask(n, fw);
-        const int cw = n >> 6;
-        const uint64_t cbit = 1ull << (n & 63);
-        uint64_t* B = a.basis + a.basis_off[c];
+// 64-bit slot s (wavefront-uniform) of a register array
+__device__ __forceinline__ uint64_t pick8(const uint64_t (&v)[kLgSlots], int s) {
+    // masked OR rather than a select chain, which the compiler would turn into an indexed (scratch) access
+    uint64_t r = 0;
+#pragma unroll
+    for (int k = 0; k < kLgSlots; ++k) {
+        const uint32_t m = 0u - static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(s) == k);
+        r |= v[k] & ((static_cast<uint64_t>(m) << 32) | m);
+    }
+    return r;
+}
 
-        if (tid < 64) sPmask[tid] = 0;
-        if (tid == 0) {
-            sContra = 0;
-            sFirst = -1;
-            sFirstCons = 0x7fffffffffffffffll;
+// per-lane value of slot lane/2 for lanes 0-15 (the output-word lanes), 0 elsewhere
+template <typename T>
+__device__ __forceinline__ T spread_slots(const T (&v)[kLgSlots], int lane) {
+    T r = 0;
+#pragma unroll
+    for (int k = 0; k < kLgSlots; ++k) r = ((lane >> 1) == k) ? v[k] : r;
+    return r;
+}
+
+// all-ones in the lanes whose bit is set in the 64-bit mask e
+__device__ __forceinline__ uint32_t lanes_of(uint64_t e, int lane) {
+    return 0u - static_cast<uint32_t>((e >> lane) & 1ull);
+}
+
+// the next half pivot word (2 pw + h) after r that holds retained pivots, or -1
+__device__ __forceinline__ int next_round(const LargeShared& L, int fw, int r) {
+    for (int t = r + 1; t < 2 * fw; ++t) {
+        const uint64_t v = L.pm[t >> 1];
+        if ((t & 1) ? (v >> 32) != 0 : (v & 0xffffffffull) != 0) return t;
+    }
+    return -1;
+}
+
+struct GroupRows {
+    uint64_t f[4];  // feature word `lane` of four retained rows (0 where absent)
+    uint64_t z[4];  // output word `lane` (lanes 0, 1) of the same rows
+};
+
+// retained rows of pivot positions q0 .. q0+3 of pivot word pw
+__device__ __forceinline__ void load_group(const uint64_t* B, int W, int fw, int n, uint64_t pmw, int pw, int q0,
+                                           int lane, GroupRows& gr) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const bool present = (pmw >> (q0 + i)) & 1ull;
+        const uint64_t* row = B + static_cast<int64_t>(prio_slot(64 * pw + q0 + i, n)) * W;
+        gr.f[i] = (present && lane < fw) ? row[lane] : 0ull;
+        gr.z[i] = (present && lane < 2) ? row[fw + lane] : 0ull;
+    }
+}
+
+// the 16 XOR combinations of four rows, entry e = rows of the set bits of e
+__device__ __forceinline__ void write_table(LargeShared& L, int base, const GroupRows& gr, int lane) {
+    const uint64_t f1 = gr.f[0], f2 = gr.f[1], f4 = gr.f[2], f8 = gr.f[3];
+    const uint64_t f3 = f1 ^ f2, f5 = f4 ^ f1, f6 = f4 ^ f2, f7 = f6 ^ f1;
+    uint64_t (*T)[64] = L.tf + base;
+    T[0][lane] = 0ull;
+    T[1][lane] = f1;
+    T[2][lane] = f2;
+    T[3][lane] = f3;
+    T[4][lane] = f4;
+    T[5][lane] = f5;
+    T[6][lane] = f6;
+    T[7][lane] = f7;
+    T[8][lane] = f8;
+    T[9][lane] = f8 ^ f1;
+    T[10][lane] = f8 ^ f2;
+    T[11][lane] = f8 ^ f3;
+    T[12][lane] = f8 ^ f4;
+    T[13][lane] = f8 ^ f5;
+    T[14][lane] = f8 ^ f6;
+    T[15][lane] = f8 ^ f7;
+    // output words: lane l < 32 writes word l & 1 of entry l >> 1
+    const int e = lane >> 1, q = lane & 1;
+    uint64_t z = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint64_t zi = q ? readlane64(gr.z[i], 1) : readlane64(gr.z[i], 0);
+        z ^= ((e >> i) & 1) ? zi : 0ull;
+    }
+    if (lane < 32) L.tz[base + e][q] = z;
+}
+
+// reduce the wavefront's block rows by the tables of half pivot word (pw, h) in buffer buf
+__device__ __forceinline__ void apply_round(const LargeShared& L, int pw, int h, int buf, uint64_t (&acc)[kLgSlots],
+                                            uint64_t& yv, int lane) {
+    const uint64_t pmw = L.pm[pw];
+    uint32_t s[kLgSlots];
+#pragma unroll
+    for (int k = 0; k < kLgSlots; ++k) s[k] = static_cast<uint32_t>((readlane64(acc[k], pw) & pmw) >> (32 * h));
+    const uint32_t sy = spread_slots(s, lane);
+    const uint32_t present = static_cast<uint32_t>(pmw >> (32 * h));
+#pragma unroll
+    for (int g = 0; g < kLgRoundTables; ++g) {
+        if (((present >> (4 * g)) & 15u) == 0) continue;
+        const int base = buf * kLgBuf + kLgEnt * g;
+#pragma unroll
+        for (int k = 0; k < kLgSlots; ++k) acc[k] ^= L.tf[base + ((s[k] >> (4 * g)) & 15u)][lane];
+        yv ^= L.tz[base + ((sy >> (4 * g)) & 15u)][lane & 1];
+    }
+}
+
+__device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& ds, LargeShared& L) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int c = ds.c;
+    const int n = ds.n;
+    const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
+    const int64_t m = ds.m;
+    const uint64_t* R = a.rows + ds.row0;
+    const uint64_t tmask = top_mask(n, fw);
+    const int cw = n >> 6;
+    const uint64_t cbit = 1ull << (n & 63);
+    uint64_t* B = a.basis + a.basis_off[c];
+    constexpr long long kNone = 0x7fffffffffffffffll;
+
+    if (tid < 64) L.pm[tid] = 0;
+    if (tid == 0) {
+        L.contra = 0;
+        L.firstMin = kNone;
+    }
+    int rank = 0;
+    int64_t b0 = 0;
+    for (; b0 < m && rank < d; b0 += kLargeRows) {
+        const int nb = static_cast<int>((m - b0) < kLargeRows ? (m - b0) : kLargeRows);
+        if (tid < 64) {
+            L.npm[tid] = 0;
+            L.rowPiv[tid] = -1;
+        }
+        if (tid == 0) L.live = 0;
+        // block rows: slot k of this wavefront is block row 8k + wave
+        uint64_t acc[kLgSlots], yv;
+#pragma unroll
+        for (int k = 0; k < kLgSlots; ++k) {
+            const int i = kLargeWaves * k + wave;
+            uint64_t v = (i < nb && lane < fw) ? R[(b0 + i) * W + lane] : 0ull;
+            acc[k] = (lane == fw - 1) ? (v & tmask) : v;
+        }
+        {
+            const int i = kLargeWaves * (lane >> 1) + wave;
+            yv = (lane < 2 * kLgSlots && i < nb) ? R[(b0 + i) * W + fw + (lane & 1)] : 0ull;
         }
         __syncthreads();
-        int rank = 0;
 
-        int64_t b0 = 0;
-        for (; b0 < m && rank < d; b0 += kLargeRows) {
-            const int nb = static_cast<int>((m - b0) < kLargeRows ? (m - b0) : kLargeRows);
-            for (int k = tid; k < nb * W; k += kLargeThreads) {
-                const int r = k / W, w = k - r * W;
-                uint64_t v = R[(b0 + r) * W + w];
-                if (w == fw - 1) v &= tmask;
-                sRow[r][w] = v;
+        // (1) block reduce against the retained basis, half a pivot word per round
+        if (rank > 0) {
+            GroupRows gr;
+            int r = next_round(L, fw, -1);
+            if (r >= 0) {
+                load_group(B, W, fw, n, L.pm[r >> 1], r >> 1, 32 * (r & 1) + 4 * wave, lane, gr);
+                write_table(L, kLgEnt * wave, gr, lane);
             }
-            if (tid == 0) sNumNew = 0;
             __syncthreads();
-
-            // (1) block reduce against the retained basis
-            if (rank > 0) {
-                uint64_t acc[kRowsPerWave], acc2[kRowsPerWave], orig[kRowsPerWave];
-#pragma unroll
-                for (int r = 0; r < kRowsPerWave; ++r) {
-                    const int i = wave + kLargeWaves * r;
-                    acc[r] = (i < nb && lane < W) ? sRow[i][lane] : 0ull;
-                    acc2[r] = (i < nb && 64 + lane < W) ? sRow[i][64 + lane] : 0ull;
-                    orig[r] = acc[r];
-                }
-                // pivot words in order, staged two at a time: the next word loads while this one is used
-                int pw = 0;
-                while (pw < fw && !sPmask[pw]) ++pw;
-                int half = 0;
-                if (pw < fw) stage_rows(reinterpret_cast<uint64_t (*)[kMaxW]>(sBuf), B, sPmask[pw], pw, n, W, wave, lane);
+            int buf = 0;
+            while (r >= 0) {
+                const int rn = next_round(L, fw, r);
+                if (rn >= 0) load_group(B, W, fw, n, L.pm[rn >> 1], rn >> 1, 32 * (rn & 1) + 4 * wave, lane, gr);
+                apply_round(L, r >> 1, r & 1, buf, acc, yv, lane);
+                if (rn >= 0) write_table(L, (buf ^ 1) * kLgBuf + kLgEnt * wave, gr, lane);
                 __syncthreads();
-                while (pw < fw) {
-                    int nx = pw + 1;
-                    while (nx < fw && !sPmask[nx]) ++nx;
-                    uint64_t (*cur)[kMaxW] = reinterpret_cast<uint64_t (*)[kMaxW]>(sBuf + half * kLargeRows * kMaxW);
-                    uint64_t (*nxt)[kMaxW] = reinterpret_cast<uint64_t (*)[kMaxW]>(sBuf + (half ^ 1) * kLargeRows * kMaxW);
-                    if (nx < fw) stage_rows(nxt, B, sPmask[nx], nx, n, W, wave, lane);
-                    const uint64_t pmw = sPmask[pw];
-                    const int cnt = __popcll(pmw);
-                    uint64_t ow[kRowsPerWave];  // pivot word pw of each unreduced row (wavefront-uniform)
-#pragma unroll
-                    for (int r = 0; r < kRowsPerWave; ++r) ow[r] = readlane64(orig[r], pw);
-                    uint64_t rest = pmw;
-                    for (int q0 = 0; q0 < cnt; q0 += 4) {
-                        int bb[4];
-                        uint64_t bv[4], bv2[4];
-#pragma unroll
-                        for (int u = 0; u < 4; ++u) {  // issue the four staged reads before using them
-                            const int q = q0 + u < cnt ? q0 + u : q0;
-                            bb[u] = (q0 + u < cnt) ? ffs64(rest) : 64;
-                            rest &= rest - 1;
-                            bv[u] = (lane < W) ? cur[q][lane] : 0ull;
-                            bv2[u] = (64 + lane < W) ? cur[q][64 + lane] : 0ull;
-                        }
-#pragma unroll
-                        for (int u = 0; u < 4; ++u) {
-#pragma unroll
-                            for (int r = 0; r < kRowsPerWave; ++r) {
-                                const uint32_t mk =
-                                    bb[u] < 64 ? static_cast<uint32_t>(0u - static_cast<uint32_t>((ow[r] >> bb[u]) & 1ull)) : 0u;
-                                acc[r] = xor_and(acc[r], mk, bv[u]);
-                                acc2[r] = xor_and(acc2[r], mk, bv2[u]);
-                            }
-                        }
-                    }
-                    __syncthreads();
-                    pw = nx;
-                    half ^= 1;
-                }
-#pragma unroll
-                for (int r = 0; r < kRowsPerWave; ++r) {
-                    const int i = wave + kLargeWaves * r;
-                    if (i < nb && lane < W) sRow[i][lane] = acc[r];
-                    if (i < nb && 64 + lane < W) sRow[i][64 + lane] = acc2[r];
-                }
-                __syncthreads();
+                r = rn;
+                buf ^= 1;
             }
+        }
 
-            // (2)+(3) in-block elimination in stream order, then the new rows are fully
-            //         reduced among themselves; one wavefront, lanes over words
-            if (wave == 0) {
-                int numNew = 0, ncon = 0;
-                long long firstc = -1;
-                for (int j = 0; j < nb; ++j) {
-                    __builtin_amdgcn_wave_barrier();  // LDS rows written by other lanes above are read below
-                    const uint64_t v = (lane < fw) ? sRow[j][lane] : 0ull;
-                    const uint64_t vx = (lane == cw) ? (v & ~cbit) : v;
-                    const uint64_t nxm = __ballot(vx != 0);
-                    const uint64_t nzm = __ballot(v != 0);
-                    int p = -1;
-                    if (nxm) {
-                        const int top = msb64(nxm);
-                        p = 64 * top + msb64(readlane64(vx, top));
-                    } else if (nzm) {
-                        p = n;
-                    }
-                    if (p < 0) {  // zero features: redundant, or contradictory with a nonzero output
-                        const bool ynz = (lane == fw || lane == fw + 1) && sRow[j][lane] != 0;
-                        if (__ballot(ynz)) {
-                            if (ncon == 0) firstc = b0 + j;
-                            ++ncon;
-                        }
-                        continue;
-                    }
-                    if (lane == 0) {
-                        sNewRow[numNew] = j;
-                        sNewPiv[numNew] = p;
-                    }
-                    ++numNew;
-                    // later rows holding bit p: one gather of that column, lane = row
-                    const int r = j + 1 + lane;
-                    uint64_t sel = __ballot(r < nb && ((sRow[r < nb ? r : j][p >> 6] >> (p & 63)) & 1ull));
-                    const uint64_t rj0 = (lane < W) ? sRow[j][lane] : 0ull;
-                    const uint64_t rj1 = (64 + lane < W) ? sRow[j][64 + lane] : 0ull;
-                    while (sel) {  // eight rows at a time: all reads, then all writes
-                        int rr[8];
-                        uint64_t t0[8], t1[8];
+        // (2) in-block elimination.  Rows whose features reduced to zero are
+        //     redundant or contradictory whatever the other block rows hold.
+        int ncon = 0;
+        long long firstc = kNone;
+        {
+            unsigned long long mine = 0;
 #pragma unroll
-                        for (int u = 0; u < 8; ++u) {
-                            rr[u] = sel ? j + 1 + ffs64(sel) : -1;
-                            sel &= sel - 1;
-                            const int rs = rr[u] < 0 ? j : rr[u];
-                            t0[u] = (lane < W) ? sRow[rs][lane] : 0ull;
-                            t1[u] = (64 + lane < W) ? sRow[rs][64 + lane] : 0ull;
-                        }
-#pragma unroll
-                        for (int u = 0; u < 8; ++u) {
-                            if (rr[u] < 0) continue;
-                            if (lane < W) sRow[rr[u]][lane] = t0[u] ^ rj0;
-                            if (64 + lane < W) sRow[rr[u]][64 + lane] = t1[u] ^ rj1;
-                        }
+            for (int k = 0; k < kLgSlots; ++k) {
+                const int i = kLargeWaves * k + wave;
+                if (__ballot(acc[k] != 0)) {
+                    mine |= 1ull << i;
+                } else if (i < nb) {
+                    if ((readlane64(yv, 2 * k) | readlane64(yv, 2 * k + 1)) != 0) {
+                        ++ncon;
+                        if (firstc == kNone) firstc = b0 + i;
                     }
                 }
-                for (int k = numNew - 1; k > 0; --k) {  // latest pivot first
-                    __builtin_amdgcn_wave_barrier();
-                    const int jk = sNewRow[k], pk = sNewPiv[k];
-                    uint64_t sel = __ballot(lane < k && ((sRow[sNewRow[lane < k ? lane : 0]][pk >> 6] >> (pk & 63)) & 1ull));
-                    const uint64_t rk0 = (lane < W) ? sRow[jk][lane] : 0ull;
-                    const uint64_t rk1 = (64 + lane < W) ? sRow[jk][64 + lane] : 0ull;
-                    while (sel) {  // eight rows at a time: all reads, then all writes
-                        int je[8];
-                        uint64_t t0[8], t1[8];
-#pragma unroll
-                        for (int u = 0; u < 8; ++u) {
-                            je[u] = sel ? sNewRow[ffs64(sel)] : -1;
-                            sel &= sel - 1;
-                            const int rs = je[u] < 0 ? jk : je[u];
-                            t0[u] = (lane < W) ? sRow[rs][lane] : 0ull;
-                            t1[u] = (64 + lane < W) ? sRow[rs][64 + lane] : 0ull;
-                        }
-#pragma unroll
-                        for (int u = 0; u < 8; ++u) {
-                            if (je[u] < 0) continue;
-                            if (lane < W) sRow[je[u]][lane] = t0[u] ^ rk0;
-                            if (64 + lane < W) sRow[je[u]][64 + lane] = t1[u] ^ rk1;
-                        }
+            }
+            if (lane == 0 && mine) atomicOr(&L.live, mine);
+        }
+        __syncthreads();
+        unsigned long long live = L.live;
+        int j = 0;
+        while (live) {
+            const int i = ffs64(live);
+            live &= live - 1;
+            const int o = i & (kLargeWaves - 1), s = i / kLargeWaves, bq = j & 1;
+            if (wave == o) {
+                const uint64_t F = pick8(acc, s);
+                const uint64_t Fx = (lane == cw) ? (F & ~cbit) : F;
+                const uint64_t nzx = __ballot(Fx != 0);
+                int p = -1;
+                if (nzx) {
+                    const int top = msb64(nzx);
+                    p = 64 * top + msb64(readlane64(Fx, top));
+                } else if (readlane64(F, cw) & cbit) {
+                    p = n;
+                }
+                const uint64_t Y0 = readlane64(yv, 2 * s), Y1 = readlane64(yv, 2 * s + 1);
+                if (p >= 0) {
+                    L.pivF[bq][lane] = F;
+                    if (lane < 2) L.pivZ[bq][lane] = lane ? Y1 : Y0;
+                    if (lane == 0) {
+                        L.rowPiv[i] = p;
+                        atomicOr(reinterpret_cast<unsigned long long*>(&L.npm[p >> 6]), 1ull << (p & 63));
                     }
+                } else if ((Y0 | Y1) != 0) {  // dependent on the earlier rows, contradictory output
+                    ++ncon;
+                    if (firstc > b0 + i) firstc = b0 + i;
+                }
+                if (lane == 0) L.pivP[bq] = p;
+            }
+            __syncthreads();
+            const int p = L.pivP[bq];
+            if (p >= 0) {
+                const uint64_t Fv = L.pivF[bq][lane];
+                const uint64_t Zv = L.pivZ[bq][lane & 1];
+                const int pw = p >> 6, pb = p & 63;
+                uint64_t em = 0;
+#pragma unroll
+                for (int k = 0; k < kLgSlots; ++k) {
+                    const bool hit = (kLargeWaves * k + wave != i) && ((readlane64(acc[k], pw) >> pb) & 1ull);
+                    const uint32_t mk = hit ? ~0u : 0u;
+                    acc[k] = xor_and(acc[k], mk, Fv);
+                    em |= hit ? (3ull << (2 * k)) : 0ull;
+                }
+                yv = xor_and(yv, lanes_of(em, lane), Zv);
+            }
+            ++j;
+        }
+        if (lane == 0 && ncon) {
+            atomicAdd(&L.contra, ncon);
+            atomicMin(&L.firstMin, firstc);
+        }
+        __syncthreads();
+
+        // (3) new rows in descending priority: position = new pivots above it
+        if (wave == 0) {
+            const uint64_t v = L.npm[lane] & ((lane == cw) ? ~cbit : ~0ull);
+            const int cnt = lane < fw ? __popcll(v) : 0;
+            int x = cnt;  // inclusive scan from the top word down
+            for (int o = 1; o < 64; o <<= 1) {
+                const int t = __shfl_down(x, o);
+                if (lane + o < 64) x += t;
+            }
+            L.above[lane] = x - cnt;
+            const int total = __shfl(x, 0) + ((L.npm[cw] & cbit) ? 1 : 0);
+            if (lane == 0) L.nnew = total;
+        }
+        __syncthreads();
+        const int K = L.nnew;
+        if (K > 0) {
+#pragma unroll
+            for (int k = 0; k < kLgSlots; ++k) {
+                const int i = kLargeWaves * k + wave;
+                const int p = L.rowPiv[i];
+                if (p < 0) continue;
+                int pos = K - 1;
+                if (p != n) {
+                    uint64_t v = L.npm[p >> 6];
+                    if ((p >> 6) == cw) v &= ~cbit;
+                    v &= (p & 63) == 63 ? 0ull : (~0ull << ((p & 63) + 1));
+                    pos = L.above[p >> 6] + __popcll(v);
+                }
+                const int e = kLgEnt * (pos >> 2) + (1 << (pos & 3));
+                L.tf[e][lane] = acc[k];
+                if ((lane >> 1) == k) L.tz[e][lane & 1] = yv;
+                if (lane == 0) L.nsorted[pos] = p;
+            }
+            __syncthreads();
+            // complete the tables: groups w and w + 8, missing rows of the last group are zero
+            const int NG = (K + 3) >> 2;
+            for (int g = wave; g < NG; g += kLargeWaves) {
+                GroupRows gr;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const bool has = 4 * g + q < K;
+                    gr.f[q] = has ? L.tf[kLgEnt * g + (1 << q)][lane] : 0ull;
+                    gr.z[q] = (has && lane < 2) ? L.tz[kLgEnt * g + (1 << q)][lane] : 0ull;
                 }
                 __builtin_amdgcn_wave_barrier();
-                for (int k = 0; k < numNew; ++k) {  // compact copy for the back-substitution and insertion
-                    const int jk = sNewRow[k];
-                    if (lane < W) sNew[k][lane] = sRow[jk][lane];
-                    if (64 + lane < W) sNew[k][64 + lane] = sRow[jk][64 + lane];
-                }
-                if (lane == 0) {
-                    sNumNew = numNew;
-                    if (ncon) {
-                        if (sContra == 0) sFirst = firstc;
-                        sContra += ncon;
-                    }
-                }
+                write_table(L, kLgEnt * g, gr, lane);
             }
             __syncthreads();
-            const int K = sNumNew;
 
-            if (K > 0) {
-                // (4) clear the new pivots from every retained row: the retained rows of each
-                //     pivot word are staged in LDS, updated there, and written back
-                for (int pw = 0; pw < fw; ++pw) {
-                    const uint64_t pmw = sPmask[pw];
-                    if (!pmw) continue;
-                    const int cnt = __popcll(pmw);
-                    uint64_t (*sStage)[kMaxW] = reinterpret_cast<uint64_t (*)[kMaxW]>(sBuf);
-                    stage_rows(sStage, B, pmw, pw, n, W, wave, lane);
-                    __syncthreads();
-                    const int pk = (lane < K) ? sNewPiv[lane] : 0;
-                    for (int q = wave; q < cnt; q += kLargeWaves) {
-                        uint64_t w0 = (lane < W) ? sStage[q][lane] : 0ull;
-                        uint64_t w1 = (64 + lane < W) ? sStage[q][64 + lane] : 0ull;
-                        const uint64_t wk = sStage[q][pk >> 6];
-                        uint64_t sel = __ballot(lane < K && ((wk >> (pk & 63)) & 1ull));
-                        while (sel) {  // eight new rows at a time, reads issued together
-                            uint64_t t0[8], t1[8];
+            // (3') clear the new pivots from the retained rows: positions wave, wave + 8, ...
+            //      of every retained pivot word, one register per row
+            const int pk = lane < K ? L.nsorted[lane] : 0;
+            const int pkw = pk >> 6, pkb = pk & 63;
+            for (int pw = 0; pw < fw; ++pw) {
+                const uint64_t pmw = L.pm[pw];
+                if (!((pmw >> wave) & 0x0101010101010101ull)) continue;
+                uint64_t Bv[kLgSlots], yb;
+                uint64_t sv[kLgSlots];
 #pragma unroll
-                            for (int u = 0; u < 8; ++u) {
-                                const int k = sel ? ffs64(sel) : -1;
-                                sel &= sel - 1;
-                                t0[u] = (k >= 0 && lane < W) ? sNew[k < 0 ? 0 : k][lane] : 0ull;
-                                t1[u] = (k >= 0 && 64 + lane < W) ? sNew[k < 0 ? 0 : k][64 + lane] : 0ull;
-                            }
-                            w0 ^= (t0[0] ^ t0[1]) ^ (t0[2] ^ t0[3]) ^ (t0[4] ^ t0[5]) ^ (t0[6] ^ t0[7]);
-                            w1 ^= (t1[0] ^ t1[1]) ^ (t1[2] ^ t1[3]) ^ (t1[4] ^ t1[5]) ^ (t1[6] ^ t1[7]);
-                        }
-                        if (lane < W) sStage[q][lane] = w0;
-                        if (64 + lane < W) sStage[q][64 + lane] = w1;
-                    }
-                    __syncthreads();
-                    unstage_rows(sStage, B, pmw, pw, n, W, wave, lane);
-                    __syncthreads();
+                for (int q = 0; q < kLgSlots; ++q) {
+                    const int b = wave + kLargeWaves * q;
+                    const bool present = (pmw >> b) & 1ull;
+                    const uint64_t* row = B + static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W;
+                    Bv[q] = (present && lane < fw) ? row[lane] : 0ull;
                 }
-                // (5) insert the new rows at their priority slots
-                for (int k = wave; k < K; k += kLargeWaves) {
-                    uint64_t* row = B + static_cast<int64_t>(prio_slot(sNewPiv[k], n)) * W;
-                    if (lane < W) row[lane] = sNew[k][lane];
-                    if (64 + lane < W) row[64 + lane] = sNew[k][64 + lane];
+                {
+                    const int q = lane >> 1, b = wave + kLargeWaves * q;
+                    const bool present = lane < 2 * kLgSlots && ((pmw >> b) & 1ull);
+                    yb = present ? B[static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W + fw + (lane & 1)] : 0ull;
                 }
-                __syncthreads();
-                if (tid == 0)
-                    for (int k = 0; k < K; ++k) sPmask[sNewPiv[k] >> 6] |= 1ull << (sNewPiv[k] & 63);
+#pragma unroll
+                for (int q = 0; q < kLgSlots; ++q) {
+                    const uint64_t wv = shfl64(Bv[q], pkw);
+                    sv[q] = __ballot(lane < K && ((wv >> pkb) & 1ull));
+                }
+                const uint64_t svy = spread_slots(sv, lane);
+                for (int g = 0; g < NG; ++g) {
+#pragma unroll
+                    for (int q = 0; q < kLgSlots; ++q) Bv[q] ^= L.tf[kLgEnt * g + ((sv[q] >> (4 * g)) & 15u)][lane];
+                    yb ^= L.tz[kLgEnt * g + ((svy >> (4 * g)) & 15u)][lane & 1];
+                }
+#pragma unroll
+                for (int q = 0; q < kLgSlots; ++q) {
+                    const int b = wave + kLargeWaves * q;
+                    if (!((pmw >> b) & 1ull)) continue;
+                    uint64_t* row = B + static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W;
+                    if (lane < fw) row[lane] = Bv[q];
+                    if ((lane >> 1) == q) row[fw + (lane & 1)] = yb;
+                }
+            }
+            // (4) insert the new rows at their priority slots
+            for (int pos = wave; pos < K; pos += kLargeWaves) {
+                const int e = kLgEnt * (pos >> 2) + (1 << (pos & 3));
+                uint64_t* row = B + static_cast<int64_t>(prio_slot(L.nsorted[pos], n)) * W;
+                if (lane < fw) row[lane] = L.tf[e][lane];
+                if (lane < 2) row[fw + lane] = L.tz[e][lane];
             }
             __syncthreads();
-            rank += K;
-        }
-
-        if (b0 < m) {
-            // full rank: every remaining row lies in the span; its residual is y + M phi
-            for (int j = tid; j < d; j += kLargeThreads) {
-                const uint64_t* row = B + static_cast<int64_t>(prio_slot(j, n)) * W;
-                sZ[j][0] = row[fw];
-                sZ[j][1] = row[fw + 1];
-            }
-            __syncthreads();
-            for (int64_t r0 = b0; r0 < m; r0 += kLargeThreads) {
-                const int64_t i = r0 + tid;
-                if (i < m) {
-                    const uint64_t* row = R + i * W;
-                    uint64_t z0 = row[fw], z1 = row[fw + 1];
-                    for (int w = 0; w < fw; ++w) {
-                        uint64_t v = row[w];
-                        if (w == fw - 1) v &= tmask;
-                        while (v) {
-                            const int jj = 64 * w + ffs64(v);
-                            v &= v - 1;
-                            z0 ^= sZ[jj][0];
-                            z1 ^= sZ[jj][1];
-                        }
-                    }
-                    if (z0 | z1) {
-                        atomicAdd(&sContra, 1);
-                        atomicMin(&sFirstCons, static_cast<long long>(i));
-                    }
-                }
-            }
-            __syncthreads();
-            if (tid == 0 && sFirst < 0 && sFirstCons != 0x7fffffffffffffffll) sFirst = sFirstCons;
-        }
-
-        // outputs: canonical map and encode table from the slots, then compaction into descending priority
-        const int64_t po = a.piv_off[c], mo = a.map_off[c];
-        for (int j = tid; j < d; j += kLargeThreads) {
-            const bool present = (sPmask[j >> 6] >> (j & 63)) & 1ull;
-            const uint64_t* row = B + static_cast<int64_t>(prio_slot(j, n)) * W;
-            a.maps[mo + 2 * j] = present ? row[fw] : 0ull;
-            a.maps[mo + 2 * j + 1] = present ? row[fw + 1] : 0ull;
-        }
-        {  // parity-check rows of the free columns: wavefront v builds words v, v + 8, ...
-            uint64_t* H = a.tables + a.basis_off[c];
-            int i = 0;
-            const bool rows = has_parity_rows(d, rank);
-            for (int w = 0; w < fw && rows; ++w) {
-                uint64_t fr = ~sPmask[w] & (w == fw - 1 ? tmask : ~0ull);
-                while (fr) {
-                    const int f = 64 * w + ffs64(fr);
-                    fr &= fr - 1;
-                    for (int v = wave; v < fw; v += kLargeWaves) {
-                        const int p = 64 * v + lane;
-                        const bool piv = (sPmask[v] >> lane) & 1ull;
-                        const bool has = piv && ((B[static_cast<int64_t>(prio_slot(p, n)) * W + w] >> (f & 63)) & 1ull);
-                        const uint64_t hv = __ballot(has) | (v == w ? (1ull << (f & 63)) : 0ull);
-                        if (lane == 0) H[static_cast<int64_t>(i) * fw + v] = hv;
-                    }
-                    ++i;
-                }
-            }
+            if (tid < 64) L.pm[tid] |= L.npm[tid];
         }
         __syncthreads();
-        for (int t0 = 0; t0 < d; t0 += kLargeWaves) {
-            const int t = t0 + wave;
-            const int pt = t < d ? slot_pivot(t, n) : 0;
-            const bool present = t < d && ((sPmask[pt >> 6] >> (pt & 63)) & 1ull);
-            uint64_t w0 = 0, w1 = 0;
-            int k = 0;
-            if (present) {
-                const uint64_t* row = B + static_cast<int64_t>(t) * W;
-                if (lane < W) w0 = row[lane];
-                if (64 + lane < W) w1 = row[64 + lane];
-                if (pt == n) {
-                    k = rank - 1;
-                } else {
-                    // pivots of higher priority: x bits above pt
-                    for (int w = pt >> 6; w < fw; ++w) {
-                        uint64_t v = sPmask[w];
-                        if (w == (pt >> 6)) v &= (pt & 63) == 63 ? 0ull : (~0ull << ((pt & 63) + 1));
-                        if (w == cw) v &= ~cbit;
-                        k += __popcll(v);
-                    }
-                }
-            }
-            __syncthreads();
-            if (present) {
-                uint64_t* out = B + static_cast<int64_t>(k) * W;
-                if (lane < W) out[lane] = w0;
-                if (64 + lane < W) out[64 + lane] = w1;
-                if (lane == 0) a.pivots[po + k] = pt;
-            }
-            __syncthreads();
-        }
-        if (tid == 0) {
-            a.rank[c] = rank;
-            a.n_contra[c] = sContra;
-            a.first_contra[c] = sFirst;
-            a.ctx_flags[c] = sContra ? F2_CTX_CONTRADICTION : 0u;
-        }
-        __syncthreads();
-      }
+        rank += K;
     }
+
+    if (b0 < m) {
+        // full rank: every remaining row lies in the span; its residual is y + M phi
+        uint64_t (*sZ)[2] = reinterpret_cast<uint64_t (*)[2]>(&L.tf[0][0]);
+        long long firstCons = kNone;
+        int ncons = 0;
+        for (int jj = tid; jj < d; jj += kLargeThreads) {
+            const uint64_t* row = B + static_cast<int64_t>(prio_slot(jj, n)) * W;
+            sZ[jj][0] = row[fw];
+            sZ[jj][1] = row[fw + 1];
+        }
+        __syncthreads();
+        for (int64_t r0 = b0; r0 < m; r0 += kLargeThreads) {
+            const int64_t i = r0 + tid;
+            if (i < m) {
+                const uint64_t* row = R + i * W;
+                uint64_t z0 = row[fw], z1 = row[fw + 1];
+                for (int w = 0; w < fw; ++w) {
+                    uint64_t v = row[w];
+                    if (w == fw - 1) v &= tmask;
+                    while (v) {
+                        const int jj = 64 * w + ffs64(v);
+                        v &= v - 1;
+                        z0 ^= sZ[jj][0];
+                        z1 ^= sZ[jj][1];
+                    }
+                }
+                if (z0 | z1) {
+                    ++ncons;
+                    if (firstCons == kNone) firstCons = i;
+                }
+            }
+        }
+        if (ncons) {
+            atomicAdd(&L.contra, ncons);
+            atomicMin(&L.firstMin, firstCons);
+        }
+        __syncthreads();
+    }
+
+    // outputs: canonical map and encode table from the slots, then compaction into descending priority
+    const int64_t po = a.piv_off[c], mo = a.map_off[c];
+    for (int jj = tid; jj < d; jj += kLargeThreads) {
+        const bool present = (L.pm[jj >> 6] >> (jj & 63)) & 1ull;
+        const uint64_t* row = B + static_cast<int64_t>(prio_slot(jj, n)) * W;
+        a.maps[mo + 2 * jj] = present ? row[fw] : 0ull;
+        a.maps[mo + 2 * jj + 1] = present ? row[fw + 1] : 0ull;
+    }
+    {  // parity-check rows of the free columns: wavefront v builds words v, v + 8, ...
+        uint64_t* H = a.tables + a.basis_off[c];
+        int i = 0;
+        const bool rows = has_parity_rows(d, rank);
+        for (int w = 0; w < fw && rows; ++w) {
+            uint64_t fr = ~L.pm[w] & (w == fw - 1 ? tmask : ~0ull);
+            while (fr) {
+                const int f = 64 * w + ffs64(fr);
+                fr &= fr - 1;
+                for (int v = wave; v < fw; v += kLargeWaves) {
+                    const int p = 64 * v + lane;
+                    const bool piv = (L.pm[v] >> lane) & 1ull;
+                    const bool has = piv && ((B[static_cast<int64_t>(prio_slot(p, n)) * W + w] >> (f & 63)) & 1ull);
+                    const uint64_t hv = __ballot(has) | (v == w ? (1ull << (f & 63)) : 0ull);
+                    if (lane == 0) H[static_cast<int64_t>(i) * fw + v] = hv;
+                }
+                ++i;
+            }
+        }
+    }
+    __syncthreads();
+    for (int t0 = 0; t0 < d; t0 += kLargeWaves) {
+        const int t = t0 + wave;
+        const int pt = t < d ? slot_pivot(t, n) : 0;
+        const bool present = t < d && ((L.pm[pt >> 6] >> (pt & 63)) & 1ull);
+        uint64_t w0 = 0, w1 = 0;
+        int k = 0;
+        if (present) {
+            const uint64_t* row = B + static_cast<int64_t>(t) * W;
+            if (lane < W) w0 = row[lane];
+            if (64 + lane < W) w1 = row[64 + lane];
+            if (pt == n) {
+                k = rank - 1;
+            } else {
+                // pivots of higher priority: x bits above pt
+                for (int w = pt >> 6; w < fw; ++w) {
+                    uint64_t v = L.pm[w];
+                    if (w == (pt >> 6)) v &= (pt & 63) == 63 ? 0ull : (~0ull << ((pt & 63) + 1));
+                    if (w == cw) v &= ~cbit;
+                    k += __popcll(v);
+                }
+            }
+        }
+        __syncthreads();
+        if (present) {
+            uint64_t* out = B + static_cast<int64_t>(k) * W;
+            if (lane < W) out[lane] = w0;
+            if (64 + lane < W) out[64 + lane] = w1;
+            if (lane == 0) a.pivots[po + k] = pt;
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        a.rank[c] = rank;
+        a.n_contra[c] = L.contra;
+        a.first_contra[c] = L.firstMin == kNone ? -1 : L.firstMin;
+        a.ctx_flags[c] = L.contra ? F2_CTX_CONTRADICTION : 0u;
+    }
+    __syncthreads();
 }
 
 // contexts of classes 1-2 (fw <= 8 beyond the register kernel: pivot-indexed LDS

@@ -79,6 +79,67 @@ def test_fit_random_large_widths(f2):
     _fit_and_compare(f2, _random_batch(77, widths, max_rows=200))
 
 
+def _large_context(rng, n, m, kind):
+    """One wide context (n >= 512) of m rows.  kind 'uniform': x uniform, y = W phi (full rank once
+    m > n, later rows run the consistency check); 'pool': x from k random generators (rank <= k, many
+    dependent rows); 'mixed': a pool prefix then uniform rows.  About 1% of rows get one output bit
+    flipped, and some rows are zero or repeat an earlier row."""
+    fw = (n + 64) // 64
+    d = n + 1
+    W = np.empty((d, 2), np.uint64)
+    W[:] = rng.integers(0, 2 ** 63, size=(d, 2), dtype=np.uint64) ^ (rng.integers(0, 2, size=(d, 2), dtype=np.uint64) << np.uint64(63))
+    rows = np.zeros((m, fw + 2), np.uint64)
+    x = rng.integers(0, 2 ** 63, size=(m, fw), dtype=np.uint64) ^ (rng.integers(0, 2, size=(m, fw), dtype=np.uint64) << np.uint64(63))
+    if kind != "uniform":
+        k = int(rng.integers(20, min(d, 400)))
+        pool = rng.integers(0, 2 ** 63, size=(k, fw), dtype=np.uint64) ^ (rng.integers(0, 2, size=(k, fw), dtype=np.uint64) << np.uint64(63))
+        cut = m if kind == "pool" else m // 2
+        for i in range(cut):
+            sel = rng.integers(0, 2, size=k).astype(bool)
+            x[i] = np.bitwise_xor.reduce(pool[sel], axis=0) if sel.any() else 0
+    vb = d - 64 * (fw - 1)
+    x[:, fw - 1] &= np.uint64((1 << vb) - 1) if vb < 64 else np.uint64((1 << 64) - 1)
+    # constant bit set on most rows (affine), cleared on a few (linear rows)
+    cw, cb = n // 64, n % 64
+    const = rng.random(m) < 0.97
+    x[const, cw] |= np.uint64(1 << cb)
+    x[~const, cw] &= ~np.uint64(1 << cb)
+    for i in np.nonzero(rng.random(m) < 0.02)[0]:
+        x[i] = 0 if rng.random() < 0.5 else x[int(rng.integers(0, i + 1))]
+    bits = np.unpackbits(x.view(np.uint8).reshape(m, fw, 8)[:, :, ::-1], axis=2).reshape(m, fw, 64)[:, :, ::-1].reshape(m, 64 * fw)[:, :d]
+    y = np.zeros((m, 2), np.uint64)
+    for j0 in range(0, d, 512):
+        blk = bits[:, j0:j0 + 512].astype(bool)
+        y ^= np.bitwise_xor.reduce(np.where(blk[:, :, None], W[None, j0:j0 + 512, :], np.uint64(0)), axis=1)
+    flip = np.nonzero(rng.random(m) < 0.01)[0]
+    for i in flip:
+        y[i, int(rng.integers(0, 2))] ^= np.uint64(1) << np.uint64(int(rng.integers(0, 64)))
+    rows[:, :fw] = x
+    rows[:, fw:] = y
+    # junk in the padding bits above the constant
+    if vb < 64:
+        rows[:, fw - 1] |= np.uint64(((1 << 64) - 1) ^ ((1 << vb) - 1)) & rng.integers(0, 2 ** 63, size=m, dtype=np.uint64)
+    return rows
+
+
+def test_fit_large_long_contexts(f2):
+    """Wide contexts over many 64-row blocks: full rank reached mid-stream (consistency phase after it),
+    rank-deficient streams with many dependent rows, contradictions before and after full rank."""
+    rng = np.random.default_rng(4242)
+    specs = [(513, 640, "uniform"), (575, 1300, "uniform"), (1000, 1100, "uniform"), (4095, 200, "uniform"),
+             (700, 900, "pool"), (2047, 1500, "pool"), (4095, 1000, "pool"), (600, 2000, "mixed"),
+             (513, 64, "pool"), (1024, 129, "uniform"), (3000, 3100, "uniform"), (1535, 1700, "mixed")]
+    n_bits, rows_list = [], []
+    for n, m, kind in specs:
+        n_bits.append(n)
+        rows_list.append(_large_context(rng, n, m, kind))
+    wl = synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+    model, ref = _fit_and_compare(f2, wl)
+    full = ref.rank == np.array([n + 1 for n in n_bits])
+    assert full.sum() >= 4 and (~full).sum() >= 4        # both regimes exercised
+    assert ((ref.flags & 1) != 0).sum() >= 6            # contradictions found
+
+
 def test_fit_degenerate_contexts(f2):
     """n=0; 0 rows; all-zero rows; zero features with nonzero output; linear (bias 0) rows; duplicates."""
     rows_list, n_bits = [], []
