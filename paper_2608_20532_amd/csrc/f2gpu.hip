@@ -29,6 +29,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "../../include/f2gpu.h"
 
 namespace {
@@ -55,7 +57,8 @@ struct FitArgs {
     uint32_t* ctx_flags;
     int32_t* n_contra;
     int64_t* first_contra;
-    int32_t* plan;  // workspace: class list offsets, dynamic counters, context lists (k_fit_plan)
+    int32_t* plan;  // workspace: class list offsets, group barrier counters, context lists (k_fit_plan)
+    int32_t coop;   // the wide kernel runs as a cooperative launch (all workgroups resident)
 };
 
 struct EncArgs {
@@ -184,7 +187,9 @@ constexpr int kRegMaxFW = 3;
 constexpr int kPivMaxFW = 8;
 constexpr int kLongRows = 256;  // contexts with more rows take the multi-wavefront kernel
 enum { kClsReg = 0, kClsPiv = 1, kClsPivLong = 2, kClsLarge = 3, kNumCls = 4 };
-constexpr int kPlanHead = 16;
+constexpr int kBarHead = 16;                // plan words kBarHead ..: barrier counters of workgroup groups
+constexpr int kMaxGroups = 128;
+constexpr int kPlanHead = kBarHead + kMaxGroups;
 constexpr int kBuckets = 256;
 constexpr int kPlanBins = kNumCls * kBuckets;
 constexpr int kPlanThreads = 1024;  // one context per thread; one bin per thread in the scan
@@ -231,6 +236,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_count(FitArgs a) {
     const int tid = threadIdx.x;
     sBin[tid] = 0;
     __syncthreads();
+    if (blockIdx.x == 0 && tid < kMaxGroups) a.plan[kBarHead + tid] = 0;
     const int64_t c = static_cast<int64_t>(blockIdx.x) * kPlanThreads + tid;
     if (c < a.num_ctx) {
         const CtxDesc ds = load_desc(a, c);
@@ -285,11 +291,14 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_scatter(FitArgs a, int bl
     }
 }
 
-// the i-th context of classes cls .. cls_last (adjacent lists) dealt to this
-// workgroup (snake order), or -1
-__device__ __forceinline__ int class_ctx(const FitArgs& a, int cls, int i, int cls_last = -1) {
+// the i-th context of classes cls .. cls_last (adjacent lists) dealt to taker g
+// of G (snake order), or -1; by default the takers are the workgroups
+__device__ __forceinline__ int class_ctx(const FitArgs& a, int cls, int i, int cls_last = -1, int G = -1, int g = -1) {
     const int lo = a.plan[cls], cnt = a.plan[(cls_last < 0 ? cls : cls_last) + 1] - lo;
-    const int G = static_cast<int>(gridDim.x), g = static_cast<int>(blockIdx.x);
+    if (G < 0) {
+        G = static_cast<int>(gridDim.x);
+        g = static_cast<int>(blockIdx.x);
+    }
     const int64_t e = static_cast<int64_t>(i) * G + ((i & 1) ? G - 1 - g : g);
     return e < cnt ? a.plan[kPlanHead + lo + static_cast<int>(e)] : -1;
 }
@@ -347,6 +356,15 @@ __device__ __forceinline__ uint64_t xor_and(uint64_t f, uint32_t m, uint64_t d) 
     const uint32_t lo = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(f), m, static_cast<uint32_t>(d), 0x78);
     const uint32_t hi =
         __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(f >> 32), m, static_cast<uint32_t>(d >> 32), 0x78);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// a ^ b ^ c: one v_bitop3 per half
+__device__ __forceinline__ uint64_t xor3(uint64_t a, uint64_t b, uint64_t c) {
+    const uint32_t lo = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(a), static_cast<uint32_t>(b),
+                                                    static_cast<uint32_t>(c), 0x96);
+    const uint32_t hi = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(a >> 32), static_cast<uint32_t>(b >> 32),
+                                                    static_cast<uint32_t>(c >> 32), 0x96);
     return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
@@ -756,7 +774,7 @@ __device__ int piv_insert(PivShared& S, int n, int d, int fw, int rank, int64_t 
 }
 
 template <int FW, int NW>
-__device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
+__device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int c = ds.c, n = ds.n, d = n + 1;
     const int fw = feat_words(n);  // <= FW; records keep FW feature words, then the two output words
@@ -898,8 +916,8 @@ __device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
 // working basis lives in the caller's basis buffer, one slot per priority
 // position (slot t holds the row whose pivot is the t-th highest-priority
 // feature), and is kept fully reduced, so the final descending-priority order is
-// an in-place compaction.  Rows go in blocks of 64, row i of a block held by
-// wavefront i mod 8:
+// an in-place compaction.  Rows go in blocks of 64, rows 8w .. 8w+7 of a block
+// held by wavefront w:
 //   (1) block reduce with Four-Russians tables (the method of Arlazarov, Dinic,
 //       Kronrod and Faradzev): the retained rows of four consecutive pivot
 //       positions give a 16-entry LDS table of all their XOR combinations, and a
@@ -907,16 +925,20 @@ __device__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds, PivShared& S) {
 //       rows, the basis being fully reduced) select the entry to add.  Eight
 //       tables (32 pivot positions) are built per round while the previous
 //       round's tables are read;
-//   (2) in-block elimination in stream order with one workgroup barrier per row:
-//       the wavefront holding the row finds its pivot and publishes the row, and
-//       every wavefront clears that pivot from the other rows it holds (earlier
-//       new rows included, so the block's new rows end fully reduced);
+//   (2) in-block elimination in stream order, one wavefront at a time over its
+//       own eight rows, each new pivot cleared from that wavefront's other rows at
+//       once and from the other wavefronts' rows after a barrier (earlier new rows
+//       included, so the block's new rows end fully reduced);
 //   (3) back-substitution: the new rows, in descending priority, form tables of
 //       four rows each, and every retained row adds the entry its bits at those
 //       pivots select; (4) the new rows are stored at their priority slots.
-// Once the rank reaches d every later row lies in the span and the basis is the
-// identity on the features, so a row's residual is y + M phi (the canonical
-// map, staged in LDS): those rows are only checked for contradictions.
+// A feature word whose columns are all retained pivots is zero in every reduced
+// row and in every new row, so steps (1) and (3) read and write only the other
+// words (the "active" lanes); the words left alone keep the unreduced bits the
+// selections are read from.  Once the rank reaches d every later row lies in the
+// span and the basis is the identity on the features, so a row's residual is
+// y + M phi (the canonical map, staged in LDS): those rows are only checked for
+// contradictions.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int prio_slot(int p, int n) { return p < n ? n - 1 - p : n; }
 __device__ __forceinline__ int slot_pivot(int t, int n) { return t < n ? n - 1 - t : n; }
@@ -932,30 +954,16 @@ static_assert(kLgRoundTables * 4 == 32, "a round covers half a pivot word");
 struct LargeShared {
     uint64_t tf[2 * kLgBuf][64];  // table entries, feature words (lane = word); the map in the full-rank phase
     uint64_t tz[2 * kLgBuf][2];   // table entries, output words
-    uint64_t pivF[2][64];         // in-block elimination: the published row
-    uint64_t pivZ[2][2];
-    int pivP[2];
+    int pubP[2][kLgSlots];        // in-block elimination: pivots published by one wavefront (tables in tf)
+    int pubN[2];
     int rowPiv[kLargeRows];       // pivot of each block row that became a basis row, else -1
     int nsorted[kLargeRows];      // the block's new pivots in descending priority
     int above[64];                // new pivots (constant excluded) in feature words above w
     uint64_t pm[64];              // pivot columns of the retained basis
     uint64_t npm[64];             // pivot columns found in the current block
-    unsigned long long live;      // block rows with a nonzero feature residual after the reduce
     int contra, nnew;
     long long firstMin;
 };
-
-// 64-bit slot s (wavefront-uniform) of a register array
-__device__ __forceinline__ uint64_t pick8(const uint64_t (&v)[kLgSlots], int s) {
-    // masked OR rather than a select chain, which the compiler would turn into an indexed (scratch) access
-    uint64_t r = 0;
-#pragma unroll
-    for (int k = 0; k < kLgSlots; ++k) {
-        const uint32_t m = 0u - static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(s) == k);
-        r |= v[k] & ((static_cast<uint64_t>(m) << 32) | m);
-    }
-    return r;
-}
 
 // per-lane value of slot lane/2 for lanes 0-15 (the output-word lanes), 0 elsewhere
 template <typename T>
@@ -971,67 +979,108 @@ __device__ __forceinline__ uint32_t lanes_of(uint64_t e, int lane) {
     return 0u - static_cast<uint32_t>((e >> lane) & 1ull);
 }
 
-// the next half pivot word (2 pw + h) after r that holds retained pivots, or -1
-__device__ __forceinline__ int next_round(const LargeShared& L, int fw, int r) {
+// the next half pivot word (2 pw + h) after r that holds retained pivots and
+// belongs to member g of a group of G (a power of 2; pivot words pw = g mod G), or -1
+__device__ __forceinline__ int next_round(const LargeShared& L, int fw, int r, int G, int g) {
     for (int t = r + 1; t < 2 * fw; ++t) {
+        if (((t >> 1) & (G - 1)) != g) continue;
         const uint64_t v = L.pm[t >> 1];
         if ((t & 1) ? (v >> 32) != 0 : (v & 0xffffffffull) != 0) return t;
     }
     return -1;
 }
 
+// barrier of the G workgroups that fit one context together (all resident: the
+// launch is cooperative); counter `bar` only grows, epoch counts this member's
+// arrivals.  The wait is bounded so that a kernel can never hang on it.
+// full: release and acquire fences around it (every earlier global write of the
+// group visible after it); otherwise only the arrival order: the data exchanged
+// across it must be written and read with device-scope atomic stores and loads.
+__device__ __forceinline__ void group_barrier(int* bar, int& epoch, int G, bool full = true) {
+    if (full) __threadfence();
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's stores performed before the arrival is counted
+    __syncthreads();
+    ++epoch;
+    if (threadIdx.x == 0) {
+        __hip_atomic_fetch_add(bar, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int target = G * epoch;
+        for (int spin = 0; spin < (1 << 24); ++spin) {
+            if (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) break;
+            __builtin_amdgcn_s_sleep(2);
+        }
+        if (full) __threadfence();
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ void put_dev(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t get_dev(const uint64_t* p) {
+    return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 struct GroupRows {
-    uint64_t f[4];  // feature word `lane` of four retained rows (0 where absent)
-    uint64_t z[4];  // output word `lane` (lanes 0, 1) of the same rows
+    uint64_t f[4];     // feature word `lane` of four retained rows, as loaded
+    uint64_t z[4];     // output word (lane & 1) of the same rows, as loaded
+    uint32_t present;  // rows that exist (bit i), wavefront-uniform
 };
 
-// retained rows of pivot positions q0 .. q0+3 of pivot word pw
-__device__ __forceinline__ void load_group(const uint64_t* B, int W, int fw, int n, uint64_t pmw, int pw, int q0,
-                                           int lane, GroupRows& gr) {
+// retained rows of pivot positions q0 .. q0+3 of round r (pivot word r/2).  The
+// loads are unconditional (in-bounds addresses) and their values are masked only
+// where they are used, so that they stay in flight across the preceding round.
+__device__ __forceinline__ void load_group(const LargeShared& L, const uint64_t* B, int W, int fw, int n, int r,
+                                           int wave, int lane, GroupRows& gr) {
+    const int pw = r >> 1, q0 = 32 * (r & 1) + 4 * wave;
+    gr.present = static_cast<uint32_t>((L.pm[pw] >> q0) & 15ull);
+    const int fl = lane < fw ? lane : 0, zl = fw + (lane & 1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const bool present = (pmw >> (q0 + i)) & 1ull;
         const uint64_t* row = B + static_cast<int64_t>(prio_slot(64 * pw + q0 + i, n)) * W;
-        gr.f[i] = (present && lane < fw) ? row[lane] : 0ull;
-        gr.z[i] = (present && lane < 2) ? row[fw + lane] : 0ull;
+        gr.f[i] = row[fl];
+        gr.z[i] = row[zl];
     }
 }
 
 // the 16 XOR combinations of four rows, entry e = rows of the set bits of e
-__device__ __forceinline__ void write_table(LargeShared& L, int base, const GroupRows& gr, int lane) {
-    const uint64_t f1 = gr.f[0], f2 = gr.f[1], f4 = gr.f[2], f8 = gr.f[3];
+__device__ __forceinline__ void write_table(LargeShared& L, int base, const GroupRows& gr, int lane, bool act) {
+    const uint64_t f1 = (act && (gr.present & 1u)) ? gr.f[0] : 0ull, f2 = (act && (gr.present & 2u)) ? gr.f[1] : 0ull;
+    const uint64_t f4 = (act && (gr.present & 4u)) ? gr.f[2] : 0ull, f8 = (act && (gr.present & 8u)) ? gr.f[3] : 0ull;
     const uint64_t f3 = f1 ^ f2, f5 = f4 ^ f1, f6 = f4 ^ f2, f7 = f6 ^ f1;
-    uint64_t (*T)[64] = L.tf + base;
-    T[0][lane] = 0ull;
-    T[1][lane] = f1;
-    T[2][lane] = f2;
-    T[3][lane] = f3;
-    T[4][lane] = f4;
-    T[5][lane] = f5;
-    T[6][lane] = f6;
-    T[7][lane] = f7;
-    T[8][lane] = f8;
-    T[9][lane] = f8 ^ f1;
-    T[10][lane] = f8 ^ f2;
-    T[11][lane] = f8 ^ f3;
-    T[12][lane] = f8 ^ f4;
-    T[13][lane] = f8 ^ f5;
-    T[14][lane] = f8 ^ f6;
-    T[15][lane] = f8 ^ f7;
+    {  // inactive lanes get zero entries, so that adding an entry leaves them unchanged
+        uint64_t (*T)[64] = L.tf + base;
+        T[0][lane] = 0ull;
+        T[1][lane] = f1;
+        T[2][lane] = f2;
+        T[3][lane] = f3;
+        T[4][lane] = f4;
+        T[5][lane] = f5;
+        T[6][lane] = f6;
+        T[7][lane] = f7;
+        T[8][lane] = f8;
+        T[9][lane] = f8 ^ f1;
+        T[10][lane] = f8 ^ f2;
+        T[11][lane] = f8 ^ f3;
+        T[12][lane] = f8 ^ f4;
+        T[13][lane] = f8 ^ f5;
+        T[14][lane] = f8 ^ f6;
+        T[15][lane] = f8 ^ f7;
+    }
     // output words: lane l < 32 writes word l & 1 of entry l >> 1
     const int e = lane >> 1, q = lane & 1;
     uint64_t z = 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const uint64_t zi = q ? readlane64(gr.z[i], 1) : readlane64(gr.z[i], 0);
+        const uint64_t zi = ((gr.present >> i) & 1u) ? (q ? readlane64(gr.z[i], 1) : readlane64(gr.z[i], 0)) : 0ull;
         z ^= ((e >> i) & 1) ? zi : 0ull;
     }
     if (lane < 32) L.tz[base + e][q] = z;
 }
 
-// reduce the wavefront's block rows by the tables of half pivot word (pw, h) in buffer buf
-__device__ __forceinline__ void apply_round(const LargeShared& L, int pw, int h, int buf, uint64_t (&acc)[kLgSlots],
-                                            uint64_t& yv, int lane) {
+// reduce the wavefront's block rows by the tables of round r in buffer buf
+__device__ __forceinline__ void apply_round(const LargeShared& L, int r, int buf, uint64_t (&acc)[kLgSlots],
+                                            uint64_t& yv, int lane, bool act) {
+    const int pw = r >> 1, h = r & 1;
     const uint64_t pmw = L.pm[pw];
     uint32_t s[kLgSlots];
 #pragma unroll
@@ -1039,23 +1088,53 @@ __device__ __forceinline__ void apply_round(const LargeShared& L, int pw, int h,
     const uint32_t sy = spread_slots(s, lane);
     const uint32_t present = static_cast<uint32_t>(pmw >> (32 * h));
 #pragma unroll
-    for (int g = 0; g < kLgRoundTables; ++g) {
-        if (((present >> (4 * g)) & 15u) == 0) continue;
-        const int base = buf * kLgBuf + kLgEnt * g;
+    for (int g = 0; g < kLgRoundTables; g += 2) {  // two tables at a time, one three-input XOR
+        if (((present >> (4 * g)) & 0xffu) == 0) continue;
+        const int b0 = buf * kLgBuf + kLgEnt * g, b1 = b0 + kLgEnt;
+        // all reads issued before the first use (entries are zero in the inactive lanes,
+        // and every table of the round is written, absent rows as zero)
+        uint64_t t0[kLgSlots], t1[kLgSlots];
 #pragma unroll
-        for (int k = 0; k < kLgSlots; ++k) acc[k] ^= L.tf[base + ((s[k] >> (4 * g)) & 15u)][lane];
-        yv ^= L.tz[base + ((sy >> (4 * g)) & 15u)][lane & 1];
+        for (int k = 0; k < kLgSlots; ++k) {
+            t0[k] = L.tf[b0 + ((s[k] >> (4 * g)) & 15u)][lane];
+            t1[k] = L.tf[b1 + ((s[k] >> (4 * g + 4)) & 15u)][lane];
+        }
+        const uint64_t ty0 = L.tz[b0 + ((sy >> (4 * g)) & 15u)][lane & 1];
+        const uint64_t ty1 = L.tz[b1 + ((sy >> (4 * g + 4)) & 15u)][lane & 1];
+#pragma unroll
+        for (int k = 0; k < kLgSlots; ++k) acc[k] = xor3(acc[k], t0[k], t1[k]);
+        yv = xor3(yv, ty0, ty1);
     }
 }
 
-__device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& ds, LargeShared& L) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// new pivot of a row (lane = word): highest-priority set feature, the constant last; -1 if none
+__device__ __forceinline__ int row_pivot(uint64_t F, int n, int cw, uint64_t cbit, int lane) {
+    const uint64_t Fx = (lane == cw) ? (F & ~cbit) : F;
+    const uint64_t nzx = __ballot(Fx != 0);
+    if (nzx) {
+        const int top = msb64(nzx);
+        return 64 * top + msb64(readlane64(Fx, top));
+    }
+    return (readlane64(F, cw) & cbit) ? n : -1;
+}
+
+// G workgroups may fit one context together (member g): each reduces the block
+// by the tables of its own pivot words and the partial sums are exchanged
+// through the context's tables buffer (free until the outputs are written); the
+// in-block elimination runs in every member on identical data; each member
+// back-substitutes and stores the rows of its own pivot words; member 0 writes
+// the outputs.
+__device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& ds, LargeShared& L, int G, int g,
+                                              int* bar, int& epoch) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c = ds.c;
     const int n = ds.n;
     const int fw = feat_words(n), W = fw + F2_Y_WORDS, d = n + 1;
     const int64_t m = ds.m;
     const uint64_t* R = a.rows + ds.row0;
     const uint64_t tmask = top_mask(n, fw);
+    const uint64_t lmask = lane < fw ? (lane == fw - 1 ? tmask : ~0ull) : 0ull;  // valid bits of word `lane`
     const int cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
     uint64_t* B = a.basis + a.basis_off[c];
@@ -1068,117 +1147,189 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
     }
     int rank = 0;
     int64_t b0 = 0;
-    for (; b0 < m && rank < d; b0 += kLargeRows) {
+    for (int blk = 0; b0 < m && rank < d; b0 += kLargeRows, ++blk) {
         const int nb = static_cast<int>((m - b0) < kLargeRows ? (m - b0) : kLargeRows);
         if (tid < 64) {
             L.npm[tid] = 0;
             L.rowPiv[tid] = -1;
         }
-        if (tid == 0) L.live = 0;
-        // block rows: slot k of this wavefront is block row 8k + wave
+        // block rows: slot k of wavefront w is block row 8w + k
         uint64_t acc[kLgSlots], yv;
 #pragma unroll
         for (int k = 0; k < kLgSlots; ++k) {
-            const int i = kLargeWaves * k + wave;
-            uint64_t v = (i < nb && lane < fw) ? R[(b0 + i) * W + lane] : 0ull;
-            acc[k] = (lane == fw - 1) ? (v & tmask) : v;
+            const int i = kLgSlots * wave + k;
+            acc[k] = (i < nb && lane < fw) ? (R[(b0 + i) * W + lane] & lmask) : 0ull;
         }
         {
-            const int i = kLargeWaves * (lane >> 1) + wave;
+            const int i = kLgSlots * wave + (lane >> 1);
             yv = (lane < 2 * kLgSlots && i < nb) ? R[(b0 + i) * W + fw + (lane & 1)] : 0ull;
         }
+        // drain the row loads here: left outstanding, they would make every later wait
+        // inside the reduce loop a wait for all memory operations
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
+        // active lanes: feature words with at least one column that is not a retained pivot
+        const bool act = lane < fw && (L.pm[lane] | ~lmask) != ~0ull;
 
         // (1) block reduce against the retained basis, half a pivot word per round
         if (rank > 0) {
-            GroupRows gr;
-            int r = next_round(L, fw, -1);
+            GroupRows gA, gB;
+            int r = next_round(L, fw, -1, G, g);
             if (r >= 0) {
-                load_group(B, W, fw, n, L.pm[r >> 1], r >> 1, 32 * (r & 1) + 4 * wave, lane, gr);
-                write_table(L, kLgEnt * wave, gr, lane);
+                load_group(L, B, W, fw, n, r, wave, lane, gA);
+                write_table(L, kLgEnt * wave, gA, lane, act);
             }
+            int rn = r >= 0 ? next_round(L, fw, r, G, g) : -1;
+            if (rn >= 0) load_group(L, B, W, fw, n, rn, wave, lane, gA);
             __syncthreads();
             int buf = 0;
             while (r >= 0) {
-                const int rn = next_round(L, fw, r);
-                if (rn >= 0) load_group(B, W, fw, n, L.pm[rn >> 1], rn >> 1, 32 * (rn & 1) + 4 * wave, lane, gr);
-                apply_round(L, r >> 1, r & 1, buf, acc, yv, lane);
-                if (rn >= 0) write_table(L, (buf ^ 1) * kLgBuf + kLgEnt * wave, gr, lane);
+                const int rnn = rn >= 0 ? next_round(L, fw, rn, G, g) : -1;
+                if (rnn >= 0) load_group(L, B, W, fw, n, rnn, wave, lane, gB);
+                apply_round(L, r, buf, acc, yv, lane, act);
+                if (rn >= 0) write_table(L, (buf ^ 1) * kLgBuf + kLgEnt * wave, gA, lane, act);
                 __syncthreads();
                 r = rn;
+                rn = rnn;
+                gA = gB;
                 buf ^= 1;
             }
+            if (G > 1) {
+                // member o holds X + P_o (X the unreduced rows, P_o its tables' sum); the
+                // reduced rows are X + sum P_o = X + sum (X + P_o) for an even G
+                uint64_t* X = a.tables + a.basis_off[c];
+                const int64_t xs = static_cast<int64_t>(kLargeRows) * W;  // one member's block
+                uint64_t* mine = X + ((blk & 1) * G + g) * xs;
+                const int yi = kLgSlots * wave + (lane >> 1);
+#pragma unroll
+                for (int k = 0; k < kLgSlots; ++k)
+                    if (act) put_dev(mine + (kLgSlots * wave + k) * W + lane, acc[k]);
+                if (lane < 2 * kLgSlots) put_dev(mine + yi * W + fw + (lane & 1), yv);
+                group_barrier(bar, epoch, G, false);
+                for (int o = 0; o < G; ++o) {
+                    if (o == g) continue;
+                    const uint64_t* other = X + ((blk & 1) * G + o) * xs;
+#pragma unroll
+                    for (int k = 0; k < kLgSlots; ++k)
+                        if (act) acc[k] ^= get_dev(other + (kLgSlots * wave + k) * W + lane);
+                    if (lane < 2 * kLgSlots) yv ^= get_dev(other + yi * W + fw + (lane & 1));
+                }
+#pragma unroll
+                for (int k = 0; k < kLgSlots; ++k) {  // + X, reloaded
+                    const int i = kLgSlots * wave + k;
+                    if (act && i < nb) acc[k] ^= R[(b0 + i) * W + lane] & lmask;
+                }
+                if (lane < 2 * kLgSlots && yi < nb) yv ^= R[(b0 + yi) * W + fw + (lane & 1)];
+            }
+#pragma unroll
+            for (int k = 0; k < kLgSlots; ++k) acc[k] = act ? acc[k] : 0ull;
         }
 
         // (2) in-block elimination.  Rows whose features reduced to zero are
         //     redundant or contradictory whatever the other block rows hold.
         int ncon = 0;
         long long firstc = kNone;
-        {
-            unsigned long long mine = 0;
+        unsigned long long mine = 0;
 #pragma unroll
-            for (int k = 0; k < kLgSlots; ++k) {
-                const int i = kLargeWaves * k + wave;
-                if (__ballot(acc[k] != 0)) {
-                    mine |= 1ull << i;
-                } else if (i < nb) {
-                    if ((readlane64(yv, 2 * k) | readlane64(yv, 2 * k + 1)) != 0) {
-                        ++ncon;
-                        if (firstc == kNone) firstc = b0 + i;
-                    }
+        for (int k = 0; k < kLgSlots; ++k) {
+            const int i = kLgSlots * wave + k;
+            if (__ballot(acc[k] != 0)) {
+                mine |= 1ull << k;
+            } else if (i < nb) {
+                if ((readlane64(yv, 2 * k) | readlane64(yv, 2 * k + 1)) != 0) {
+                    ++ncon;
+                    if (firstc == kNone) firstc = b0 + i;
                 }
             }
-            if (lane == 0 && mine) atomicOr(&L.live, mine);
         }
-        __syncthreads();
-        unsigned long long live = L.live;
-        int j = 0;
-        while (live) {
-            const int i = ffs64(live);
-            live &= live - 1;
-            const int o = i & (kLargeWaves - 1), s = i / kLargeWaves, bq = j & 1;
-            if (wave == o) {
-                const uint64_t F = pick8(acc, s);
-                const uint64_t Fx = (lane == cw) ? (F & ~cbit) : F;
-                const uint64_t nzx = __ballot(Fx != 0);
-                int p = -1;
-                if (nzx) {
-                    const int top = msb64(nzx);
-                    p = 64 * top + msb64(readlane64(Fx, top));
-                } else if (readlane64(F, cw) & cbit) {
-                    p = n;
-                }
-                const uint64_t Y0 = readlane64(yv, 2 * s), Y1 = readlane64(yv, 2 * s + 1);
-                if (p >= 0) {
-                    L.pivF[bq][lane] = F;
-                    if (lane < 2) L.pivZ[bq][lane] = lane ? Y1 : Y0;
+        for (int ph = 0; ph < kLargeWaves; ++ph) {
+            const int bq = ph & 1;
+            const int tb = 2 * kLgEnt * bq;  // this phase's two tables in tf (the reduce is done with it)
+            if (wave == ph) {  // this wavefront's rows in order; earlier wavefronts' pivots already applied
+                unsigned newSlots = 0;
+#pragma unroll
+                for (int s = 0; s < kLgSlots; ++s) {
+                    if (!((mine >> s) & 1ull)) continue;
+                    const int i = kLgSlots * ph + s;
+                    const uint64_t F = acc[s];
+                    const int p = row_pivot(F, n, cw, cbit, lane);
+                    const uint64_t Y0 = readlane64(yv, 2 * s), Y1 = readlane64(yv, 2 * s + 1);
+                    if (p < 0) {  // dependent on the earlier rows: redundant, or contradictory
+                        if ((Y0 | Y1) != 0) {
+                            ++ncon;
+                            if (firstc > b0 + i) firstc = b0 + i;
+                        }
+                        continue;
+                    }
+                    const int pw = p >> 6, pb = p & 63;
+                    uint64_t em = 0;
+#pragma unroll
+                    for (int t = 0; t < kLgSlots; ++t) {
+                        if (t == s) continue;
+                        const bool hit = (readlane64(acc[t], pw) >> pb) & 1ull;
+                        acc[t] = xor_and(acc[t], hit ? ~0u : 0u, F);
+                        em |= hit ? (3ull << (2 * t)) : 0ull;
+                    }
+                    yv = xor_and(yv, lanes_of(em, lane), (lane & 1) ? Y1 : Y0);
+                    newSlots |= 1u << s;
                     if (lane == 0) {
                         L.rowPiv[i] = p;
-                        atomicOr(reinterpret_cast<unsigned long long*>(&L.npm[p >> 6]), 1ull << (p & 63));
+                        atomicOr(reinterpret_cast<unsigned long long*>(&L.npm[pw]), 1ull << pb);
                     }
-                } else if ((Y0 | Y1) != 0) {  // dependent on the earlier rows, contradictory output
-                    ++ncon;
-                    if (firstc > b0 + i) firstc = b0 + i;
                 }
-                if (lane == 0) L.pivP[bq] = p;
+                // the new rows, now fully reduced among themselves, as two 4-row tables
+                const int np = __popc(newSlots);
+#pragma unroll
+                for (int s = 0; s < kLgSlots; ++s) {
+                    if (!((newSlots >> s) & 1u)) continue;
+                    const int q = __popc(newSlots & ((1u << s) - 1u));
+                    const int e = tb + kLgEnt * (q >> 2) + (1 << (q & 3));
+                    L.tf[e][lane] = acc[s];
+                    if ((lane >> 1) == s) L.tz[e][lane & 1] = yv;
+                    if (lane == 0) L.pubP[bq][q] = L.rowPiv[kLgSlots * ph + s];
+                }
+                wave_sync();
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    GroupRows gr;
+                    gr.present = 0;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const bool has = 4 * t + q < np;
+                        gr.present |= has ? (1u << q) : 0u;
+                        gr.f[q] = has ? L.tf[tb + kLgEnt * t + (1 << q)][lane] : 0ull;
+                        gr.z[q] = has ? L.tz[tb + kLgEnt * t + (1 << q)][lane & 1] : 0ull;
+                    }
+                    wave_sync();
+                    write_table(L, tb + kLgEnt * t, gr, lane, true);
+                }
+                if (lane == 0) L.pubN[bq] = np;
             }
             __syncthreads();
-            const int p = L.pivP[bq];
-            if (p >= 0) {
-                const uint64_t Fv = L.pivF[bq][lane];
-                const uint64_t Zv = L.pivZ[bq][lane & 1];
-                const int pw = p >> 6, pb = p & 63;
-                uint64_t em = 0;
+            const int np = L.pubN[bq];
+            if (wave != ph && np > 0) {  // the published rows: selection bits at their pivots, one entry per table
+                const int pk = lane < np ? L.pubP[bq][lane] : 0;
+                const int pkw = pk >> 6, pkb = pk & 63;
+                uint32_t sel[kLgSlots];
+                uint64_t wv[kLgSlots];
+#pragma unroll
+                for (int k = 0; k < kLgSlots; ++k) wv[k] = shfl64(acc[k], pkw);
+#pragma unroll
+                for (int k = 0; k < kLgSlots; ++k)
+                    sel[k] = static_cast<uint32_t>(__ballot(lane < np && ((wv[k] >> pkb) & 1ull)));
+                const uint32_t sy = spread_slots(sel, lane);
+                uint64_t t0[kLgSlots], t1[kLgSlots];
 #pragma unroll
                 for (int k = 0; k < kLgSlots; ++k) {
-                    const bool hit = (kLargeWaves * k + wave != i) && ((readlane64(acc[k], pw) >> pb) & 1ull);
-                    const uint32_t mk = hit ? ~0u : 0u;
-                    acc[k] = xor_and(acc[k], mk, Fv);
-                    em |= hit ? (3ull << (2 * k)) : 0ull;
+                    t0[k] = L.tf[tb + (sel[k] & 15u)][lane];
+                    t1[k] = L.tf[tb + kLgEnt + ((sel[k] >> 4) & 15u)][lane];
                 }
-                yv = xor_and(yv, lanes_of(em, lane), Zv);
+                const uint64_t ty0 = L.tz[tb + (sy & 15u)][lane & 1];
+                const uint64_t ty1 = L.tz[tb + kLgEnt + ((sy >> 4) & 15u)][lane & 1];
+#pragma unroll
+                for (int k = 0; k < kLgSlots; ++k) acc[k] = xor3(acc[k], t0[k], t1[k]);
+                yv = xor3(yv, ty0, ty1);
             }
-            ++j;
         }
         if (lane == 0 && ncon) {
             atomicAdd(&L.contra, ncon);
@@ -1204,7 +1355,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
         if (K > 0) {
 #pragma unroll
             for (int k = 0; k < kLgSlots; ++k) {
-                const int i = kLargeWaves * k + wave;
+                const int i = kLgSlots * wave + k;
                 const int p = L.rowPiv[i];
                 if (p < 0) continue;
                 int pos = K - 1;
@@ -1224,60 +1375,85 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
             const int NG = (K + 3) >> 2;
             for (int g = wave; g < NG; g += kLargeWaves) {
                 GroupRows gr;
+                gr.present = 0;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const bool has = 4 * g + q < K;
+                    gr.present |= has ? (1u << q) : 0u;
                     gr.f[q] = has ? L.tf[kLgEnt * g + (1 << q)][lane] : 0ull;
-                    gr.z[q] = (has && lane < 2) ? L.tz[kLgEnt * g + (1 << q)][lane] : 0ull;
+                    gr.z[q] = has ? L.tz[kLgEnt * g + (1 << q)][lane & 1] : 0ull;
                 }
                 __builtin_amdgcn_wave_barrier();
-                write_table(L, kLgEnt * g, gr, lane);
+                write_table(L, kLgEnt * g, gr, lane, true);
             }
             __syncthreads();
 
             // (3') clear the new pivots from the retained rows: positions wave, wave + 8, ...
-            //      of every retained pivot word, one register per row
+            //      of every retained pivot word, one register per row, the next word's rows
+            //      loaded while this word's are updated
             const int pk = lane < K ? L.nsorted[lane] : 0;
             const int pkw = pk >> 6, pkb = pk & 63;
-            for (int pw = 0; pw < fw; ++pw) {
-                const uint64_t pmw = L.pm[pw];
-                if (!((pmw >> wave) & 0x0101010101010101ull)) continue;
-                uint64_t Bv[kLgSlots], yb;
-                uint64_t sv[kLgSlots];
+            const uint64_t mineBits = 0x0101010101010101ull << wave;
+            auto next_word = [&](int pw) {  // this member's pivot words only
+                for (++pw; pw < fw; ++pw)
+                    if ((pw & (G - 1)) == g && (L.pm[pw] & mineBits)) return pw;
+                return -1;
+            };
+            auto load_rows = [&](int pw, uint64_t (&Bv)[kLgSlots], uint64_t& yb) {  // raw: masked where used
 #pragma unroll
                 for (int q = 0; q < kLgSlots; ++q) {
                     const int b = wave + kLargeWaves * q;
-                    const bool present = (pmw >> b) & 1ull;
-                    const uint64_t* row = B + static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W;
-                    Bv[q] = (present && lane < fw) ? row[lane] : 0ull;
+                    Bv[q] = B[static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W + (lane < fw ? lane : 0)];
                 }
-                {
-                    const int q = lane >> 1, b = wave + kLargeWaves * q;
-                    const bool present = lane < 2 * kLgSlots && ((pmw >> b) & 1ull);
-                    yb = present ? B[static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W + fw + (lane & 1)] : 0ull;
-                }
+                const int b = wave + kLargeWaves * ((lane >> 1) & 7);
+                yb = B[static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W + fw + (lane & 1)];
+            };
+            uint64_t Bv[kLgSlots], yb, Bn[kLgSlots], ybn;
+            int pw = next_word(-1);
+            if (pw >= 0) load_rows(pw, Bv, yb);
+            while (pw >= 0) {
+                const int pwn = next_word(pw);
+                if (pwn >= 0) load_rows(pwn, Bn, ybn);
+                const uint64_t pmw = L.pm[pw];
 #pragma unroll
-                for (int q = 0; q < kLgSlots; ++q) {
-                    const uint64_t wv = shfl64(Bv[q], pkw);
-                    sv[q] = __ballot(lane < K && ((wv >> pkb) & 1ull));
-                }
+                for (int q = 0; q < kLgSlots; ++q) Bv[q] = (act && ((pmw >> (wave + kLargeWaves * q)) & 1ull)) ? Bv[q] : 0ull;
+                yb = (lane < 2 * kLgSlots && ((pmw >> (wave + kLargeWaves * (lane >> 1))) & 1ull)) ? yb : 0ull;
+                uint64_t sv[kLgSlots], wv[kLgSlots];
+#pragma unroll
+                for (int q = 0; q < kLgSlots; ++q) wv[q] = shfl64(Bv[q], pkw);  // all exchanges in flight together
+#pragma unroll
+                for (int q = 0; q < kLgSlots; ++q) sv[q] = __ballot(lane < K && ((wv[q] >> pkb) & 1ull));
                 const uint64_t svy = spread_slots(sv, lane);
-                for (int g = 0; g < NG; ++g) {
+                for (int g = 0; g < NG; g += 2) {  // two tables at a time (the second may not exist)
+                    const bool two = g + 1 < NG;
+                    uint64_t t0[kLgSlots], t1[kLgSlots];
 #pragma unroll
-                    for (int q = 0; q < kLgSlots; ++q) Bv[q] ^= L.tf[kLgEnt * g + ((sv[q] >> (4 * g)) & 15u)][lane];
-                    yb ^= L.tz[kLgEnt * g + ((svy >> (4 * g)) & 15u)][lane & 1];
+                    for (int q = 0; q < kLgSlots; ++q) {
+                        t0[q] = L.tf[kLgEnt * g + ((sv[q] >> (4 * g)) & 15u)][lane];
+                        t1[q] = two ? L.tf[kLgEnt * (g + 1) + ((sv[q] >> (4 * g + 4)) & 15u)][lane] : 0ull;
+                    }
+                    const uint64_t ty0 = L.tz[kLgEnt * g + ((svy >> (4 * g)) & 15u)][lane & 1];
+                    const uint64_t ty1 = two ? L.tz[kLgEnt * (g + 1) + ((svy >> (4 * g + 4)) & 15u)][lane & 1] : 0ull;
+#pragma unroll
+                    for (int q = 0; q < kLgSlots; ++q) Bv[q] = xor3(Bv[q], t0[q], t1[q]);
+                    yb = xor3(yb, ty0, ty1);
                 }
 #pragma unroll
                 for (int q = 0; q < kLgSlots; ++q) {
                     const int b = wave + kLargeWaves * q;
                     if (!((pmw >> b) & 1ull)) continue;
                     uint64_t* row = B + static_cast<int64_t>(prio_slot(64 * pw + b, n)) * W;
-                    if (lane < fw) row[lane] = Bv[q];
+                    if (act) row[lane] = Bv[q];
                     if ((lane >> 1) == q) row[fw + (lane & 1)] = yb;
                 }
+                pw = pwn;
+#pragma unroll
+                for (int q = 0; q < kLgSlots; ++q) Bv[q] = Bn[q];
+                yb = ybn;
             }
-            // (4) insert the new rows at their priority slots
+            // (4) insert the new rows at their priority slots (every word: fresh slots)
             for (int pos = wave; pos < K; pos += kLargeWaves) {
+                if (((L.nsorted[pos] >> 6) & (G - 1)) != g) continue;  // another member's pivot word
                 const int e = kLgEnt * (pos >> 2) + (1 << (pos & 3));
                 uint64_t* row = B + static_cast<int64_t>(prio_slot(L.nsorted[pos], n)) * W;
                 if (lane < fw) row[lane] = L.tf[e][lane];
@@ -1290,8 +1466,10 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
         rank += K;
     }
 
+    if (G > 1) group_barrier(bar, epoch, G);  // every member's basis rows written
     if (b0 < m) {
         // full rank: every remaining row lies in the span; its residual is y + M phi
+        // (members of a group take every G-th 512-row chunk)
         uint64_t (*sZ)[2] = reinterpret_cast<uint64_t (*)[2]>(&L.tf[0][0]);
         long long firstCons = kNone;
         int ncons = 0;
@@ -1301,7 +1479,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
             sZ[jj][1] = row[fw + 1];
         }
         __syncthreads();
-        for (int64_t r0 = b0; r0 < m; r0 += kLargeThreads) {
+        for (int64_t r0 = b0 + static_cast<int64_t>(g) * kLargeThreads; r0 < m; r0 += static_cast<int64_t>(G) * kLargeThreads) {
             const int64_t i = r0 + tid;
             if (i < m) {
                 const uint64_t* row = R + i * W;
@@ -1322,12 +1500,43 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
                 }
             }
         }
-        if (ncons) {
-            atomicAdd(&L.contra, ncons);
-            atomicMin(&L.firstMin, firstCons);
+        if (G == 1) {
+            if (ncons) {
+                atomicAdd(&L.contra, ncons);
+                atomicMin(&L.firstMin, firstCons);
+            }
+            __syncthreads();
+        } else {  // members' counts through the exchange area, combined by member 0
+            __shared__ int sCnt;
+            __shared__ long long sFirst;
+            if (tid == 0) {
+                sCnt = 0;
+                sFirst = kNone;
+            }
+            __syncthreads();
+            if (ncons) {
+                atomicAdd(&sCnt, ncons);
+                atomicMin(&sFirst, firstCons);
+            }
+            __syncthreads();
+            int64_t* X = reinterpret_cast<int64_t*>(a.tables + a.basis_off[c]);
+            if (tid == 0) {
+                X[2 * g] = sCnt;
+                X[2 * g + 1] = sFirst;
+            }
+            group_barrier(bar, epoch, G);
+            if (g == 0 && tid == 0) {
+                for (int o = 1; o < G; ++o) {
+                    L.contra += static_cast<int>(X[2 * o]);
+                    if (X[2 * o + 1] < L.firstMin) L.firstMin = X[2 * o + 1];
+                }
+                L.contra += sCnt;
+                if (sFirst < L.firstMin) L.firstMin = sFirst;
+            }
+            __syncthreads();
         }
-        __syncthreads();
     }
+    if (g != 0) return;  // member 0 writes the outputs
 
     // outputs: canonical map and encode table from the slots, then compaction into descending priority
     const int64_t po = a.piv_off[c], mo = a.map_off[c];
@@ -1357,37 +1566,67 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
             }
         }
     }
+    // pivots, and the basis rows moved from their slots to positions 0 .. rank-1: the
+    // row of slot t goes to position (present slots before t) <= t, so slots are moved
+    // in increasing order, 64 at a time (read all, barrier, write all)
+    if (wave == 0) {  // present slots in words above w (slot order = descending feature index, constant last)
+        const uint64_t v = L.pm[lane] & ((lane == cw) ? ~cbit : ~0ull);
+        const int cnt = lane < fw ? __popcll(v) : 0;
+        int x = cnt;
+        for (int o = 1; o < 64; o <<= 1) {
+            const int t = __shfl_down(x, o);
+            if (lane + o < 64) x += t;
+        }
+        L.above[lane] = x - cnt;
+    }
     __syncthreads();
-    for (int t0 = 0; t0 < d; t0 += kLargeWaves) {
-        const int t = t0 + wave;
-        const int pt = t < d ? slot_pivot(t, n) : 0;
-        const bool present = t < d && ((L.pm[pt >> 6] >> (pt & 63)) & 1ull);
-        uint64_t w0 = 0, w1 = 0;
-        int k = 0;
-        if (present) {
-            const uint64_t* row = B + static_cast<int64_t>(t) * W;
-            if (lane < W) w0 = row[lane];
-            if (64 + lane < W) w1 = row[64 + lane];
-            if (pt == n) {
-                k = rank - 1;
-            } else {
-                // pivots of higher priority: x bits above pt
-                for (int w = pt >> 6; w < fw; ++w) {
-                    uint64_t v = L.pm[w];
-                    if (w == (pt >> 6)) v &= (pt & 63) == 63 ? 0ull : (~0ull << ((pt & 63) + 1));
-                    if (w == cw) v &= ~cbit;
-                    k += __popcll(v);
+    if (rank < d) {
+        for (int t0 = 0; t0 < d; t0 += kLargeRows) {
+            uint64_t w0[kLgSlots], w1[kLgSlots];
+            int kk[kLgSlots];
+#pragma unroll
+            for (int q = 0; q < kLgSlots; ++q) {
+                const int t = t0 + kLgSlots * wave + q;
+                const int pt = t < d ? slot_pivot(t, n) : 0;
+                const bool present = t < d && ((L.pm[pt >> 6] >> (pt & 63)) & 1ull);
+                kk[q] = -1;
+                w0[q] = w1[q] = 0;
+                if (present) {
+                    const uint64_t* row = B + static_cast<int64_t>(t) * W;
+                    if (lane < W) w0[q] = row[lane];
+                    if (64 + lane < W) w1[q] = row[64 + lane];
+                    if (pt == n) {
+                        kk[q] = rank - 1;
+                    } else {
+                        uint64_t v = L.pm[pt >> 6];
+                        if ((pt >> 6) == cw) v &= ~cbit;
+                        v &= (pt & 63) == 63 ? 0ull : (~0ull << ((pt & 63) + 1));
+                        kk[q] = L.above[pt >> 6] + __popcll(v);
+                    }
                 }
             }
+            __syncthreads();
+#pragma unroll
+            for (int q = 0; q < kLgSlots; ++q) {
+                if (kk[q] < 0) continue;
+                uint64_t* out = B + static_cast<int64_t>(kk[q]) * W;
+                if (lane < W) out[lane] = w0[q];
+                if (64 + lane < W) out[64 + lane] = w1[q];
+            }
+            __syncthreads();
         }
-        __syncthreads();
-        if (present) {
-            uint64_t* out = B + static_cast<int64_t>(k) * W;
-            if (lane < W) out[lane] = w0;
-            if (64 + lane < W) out[64 + lane] = w1;
-            if (lane == 0) a.pivots[po + k] = pt;
+    }
+    for (int t = tid; t < d; t += kLargeThreads) {  // full rank: every slot present, position = slot
+        const int pt = slot_pivot(t, n);
+        if (!((L.pm[pt >> 6] >> (pt & 63)) & 1ull)) continue;
+        int k = rank - 1;
+        if (pt != n) {
+            uint64_t v = L.pm[pt >> 6];
+            if ((pt >> 6) == cw) v &= ~cbit;
+            v &= (pt & 63) == 63 ? 0ull : (~0ull << ((pt & 63) + 1));
+            k = L.above[pt >> 6] + __popcll(v);
         }
-        __syncthreads();
+        a.pivots[po + k] = pt;
     }
     if (tid == 0) {
         a.rank[c] = rank;
@@ -1407,8 +1646,29 @@ union WideShared {
     LargeShared large;
 };
 
+// Wide contexts first: with few of them (as many as a quarter of the workgroups
+// or fewer) each is fitted by a group of 4 workgroups, by 2 with up to half,
+// else by one.  Under a cooperative launch every workgroup is resident, which the
+// group barriers need; otherwise groups are single workgroups.  A group's
+// workgroups are blockIdx values congruent mod 8, which the dispatcher places on
+// one die (shared L2 for the exchange).
 __global__ __launch_bounds__(kLargeThreads) void k_fit_wide(FitArgs a) {
     __shared__ WideShared U;
+    {
+        const int nl = a.plan[kClsLarge + 1] - a.plan[kClsLarge];
+        const int nwg = static_cast<int>(gridDim.x);
+        int G = 1;
+        if (a.coop && nwg % 32 == 0 && nwg / 4 <= kMaxGroups && 4 * nl <= nwg) G = 4;
+        else if (a.coop && nwg % 16 == 0 && nwg / 2 <= kMaxGroups && 2 * nl <= nwg) G = 2;
+        const int x = static_cast<int>(blockIdx.x), idx = x / 8;
+        const int g = idx % G, grp = (x % 8) + 8 * (idx / G), ngrp = nwg / G;
+        int epoch = 0;
+        for (int i = 0;; ++i) {
+            const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsLarge, i, -1, ngrp, grp));
+            if (c < 0) break;
+            fit_ctx_large(a, readlane_desc(load_desc(a, c), 0), U.large, G, g, a.plan + kBarHead + grp, epoch);
+        }
+    }
     // classes 1 and 2 are adjacent in the plan: one list of LDS-basis contexts
     for (int i = 0;; ++i) {
         const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsPiv, i, kClsPivLong));
@@ -1420,11 +1680,6 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_wide(FitArgs a) {
             case 3: case 4: fit_ctx_piv<4, kPivWaves>(a, ds, U.piv); break;
             default: fit_ctx_piv<8, kPivWaves>(a, ds, U.piv); break;
         }
-    }
-    for (int i = 0;; ++i) {
-        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsLarge, i));
-        if (c < 0) break;
-        fit_ctx_large(a, readlane_desc(load_desc(a, c), 0), U.large);
     }
 }
 
@@ -2068,17 +2323,53 @@ FitArgs fit_args(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     a.n_contra = m->n_contra;
     a.first_contra = m->first_contra_row;
     a.plan = plan;
+    a.coop = 0;
     return a;
 }
 
 // the fit: plan (two kernels), then the class kernels, each keeping about as
 // many workgroups as fit on the chip at once
-void launch_fit(const FitArgs& a, hipStream_t s) {
+// workgroups of the wide kernel that can be resident at once on the current
+// device, or 0 where cooperative launches are unavailable (queried once per device)
+int wide_resident_workgroups() {
+    static std::atomic<int> cache[64];  // value + 1; 0 = not queried yet
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+    if (dev < 64) {
+        const int v = cache[dev].load(std::memory_order_relaxed);
+        if (v > 0) return v - 1;
+    }
+    int coop = 0, cus = 0, per_cu = 0;
+    int r = 0;
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess && coop &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(k_fit_wide), kLargeThreads,
+                                                     0) == hipSuccess)
+        r = cus * per_cu;
+    (void)hipGetLastError();
+    if (dev < 64) cache[dev].store(r + 1, std::memory_order_relaxed);
+    return r;
+}
+
+// the fit: plan (two kernels), then the class kernels.  The wide kernel runs one
+// workgroup per compute unit as a cooperative launch (so that a group of
+// workgroups can fit one context together), else a plain launch of up to 256.
+void launch_fit(FitArgs a, hipStream_t s) {
     const int32_t C = a.num_ctx;
     const int plan_blocks = static_cast<int>((static_cast<int64_t>(C) + kPlanThreads - 1) / kPlanThreads);
     hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
     hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
     hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid((C + kRegWaves - 1) / kRegWaves, 256)), dim3(64 * kRegWaves), 0, s, a);
+    const int res = wide_resident_workgroups();
+    if (res >= 32) {
+        a.coop = 1;
+        void* args[] = {&a};
+        if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(k_fit_wide), dim3(res < 1024 ? res : 1024),
+                                       dim3(kLargeThreads), args, 0, s) == hipSuccess)
+            return;
+        (void)hipGetLastError();
+    }
+    a.coop = 0;
     hipLaunchKernelGGL(k_fit_wide, dim3(fit_grid(C, 256)), dim3(kLargeThreads), 0, s, a);
 }
 
