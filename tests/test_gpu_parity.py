@@ -140,6 +140,21 @@ def test_fit_large_long_contexts(f2):
     assert ((ref.flags & 1) != 0).sum() >= 6            # contradictions found
 
 
+@pytest.mark.parametrize("num_ctx", [100, 200])
+def test_fit_many_wide_contexts(f2, num_ctx):
+    """More wide contexts than a quarter (100) or half (200) of the workgroups: each context is then
+    fitted by 2 workgroups or by 1, instead of 4."""
+    rng = np.random.default_rng(num_ctx)
+    n_bits, rows_list = [], []
+    for c in range(num_ctx):
+        n = int(rng.integers(512, 900))
+        m = int(rng.integers(60, 700))
+        n_bits.append(n)
+        rows_list.append(_large_context(rng, n, m, ["uniform", "pool", "mixed"][c % 3]))
+    wl = synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+    _fit_and_compare(f2, wl)
+
+
 def test_fit_degenerate_contexts(f2):
     """n=0; 0 rows; all-zero rows; zero features with nonzero output; linear (bias 0) rows; duplicates."""
     rows_list, n_bits = [], []
