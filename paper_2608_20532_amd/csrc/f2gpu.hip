@@ -59,6 +59,7 @@ struct FitArgs {
     int64_t* first_contra;
     int32_t* plan;  // workspace: class list offsets, group barrier counters, context lists (k_fit_plan)
     int32_t coop;   // the wide kernel runs as a cooperative launch (all workgroups resident)
+    int32_t max_n;  // host hint: largest width of the batch, -1 if unknown
 };
 
 struct EncArgs {
@@ -2324,6 +2325,7 @@ FitArgs fit_args(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     a.first_contra = m->first_contra_row;
     a.plan = plan;
     a.coop = 0;
+    a.max_n = m->max_n_bits;
     return a;
 }
 
@@ -2360,7 +2362,9 @@ void launch_fit(FitArgs a, hipStream_t s) {
     hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
     hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
     hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid((C + kRegWaves - 1) / kRegWaves, 256)), dim3(64 * kRegWaves), 0, s, a);
-    const int res = wide_resident_workgroups();
+    // a batch known to hold no context wider than 8 feature words gains nothing
+    // from the cooperative launch (which costs tens of microseconds of setup)
+    const int res = (a.max_n >= 0 && a.max_n < 512) ? 0 : wide_resident_workgroups();
     if (res >= 32) {
         a.coop = 1;
         void* args[] = {&a};

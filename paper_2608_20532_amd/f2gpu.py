@@ -48,6 +48,7 @@ class f2_model(ctypes.Structure):
         ("ctx_flags", ctypes.c_void_p),
         ("n_contra", ctypes.c_void_p),
         ("first_contra_row", ctypes.c_void_p),
+        ("max_n_bits", ctypes.c_int32),
     ]
 
 
@@ -154,7 +155,8 @@ class Model:
                 int(self.basis_off_host[-1]), int(self.piv_off_host[-1]), int(self.map_off_host[-1]),
                 _ptr(self.basis), _ptr(self.pivots), _ptr(self.maps), _ptr(self.tables), _ptr(self.rank),
                 _ptr(self.ctx_flags),
-                _ptr(self.n_contra), _ptr(self.first_contra_row))
+                _ptr(self.n_contra), _ptr(self.first_contra_row),
+                int(self.n_bits_host.max()) if self.num_ctx else 0)
         return self._struct
 
 
