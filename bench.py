@@ -113,6 +113,18 @@ def load_traffic(workload):
     return phases, None
 
 
+def measured_traffic(workload, phase, roof):
+    """Add the measured HBM bytes per call of a phase (or why there are none) to a roofline object."""
+    traffic, why = load_traffic(workload)
+    tr = traffic.get(phase) if traffic else None
+    roof["traffic"] = tr["bytes"] if tr else None
+    if tr:
+        roof["kernels"] = tr["kernels"]
+    else:
+        roof["traffic_note"] = why or f"no counters for the {phase} phase of this workload"
+    return roof
+
+
 def sub_workload(wl, c0, c1):
     """Contexts [c0, c1) of a workload as (rows, row_off, n_bits) with rebased offsets."""
     off = wl.row_off[c0:c1 + 1]
@@ -228,9 +240,10 @@ def bench_stream(args):
         "ms_per_step": 1e3 * wall / args.steps, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "u64", "data": "synthetic",
         "config": {"workload": desc, "name": args.workload, "items": count},
-        "roofline": {"bound": "hbm", "kernel": kernel, "achieved": gbps, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gbps / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes, "avg_ms": ms,
-                     "traffic_note": "no counters for this workload"},
+        "roofline": measured_traffic(args.workload, args.workload,
+                                     {"bound": "hbm", "kernel": kernel, "achieved": gbps, "peak": HBM_PEAK_GBS,
+                                      "unit": "GB/s", "frac": gbps / HBM_PEAK_GBS, "algorithmic_bytes": nbytes,
+                                      "avg_ms": ms}),
         "cpu_baseline": cpu,
     }), flush=True)
 
@@ -306,9 +319,10 @@ def bench_pool(args):
         "vs_baseline": None, "dtype": "u64", "data": "synthetic",
         "config": {"workload": desc, "name": "pool", "pools": C0, "member_contexts": parts * C0,
                    "member_basis_rows": rows_in, "shared_pools": shared},
-        "roofline": {"bound": "hbm", "kernel": "f2_pool_bases", "achieved": gbps, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": gbps / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes": nbytes,
-                     "avg_ms": ms, "traffic_note": "no counters for this workload"},
+        "roofline": measured_traffic("pool", "pool",
+                                     {"bound": "hbm", "kernel": "f2_pool_bases", "achieved": gbps, "peak": HBM_PEAK_GBS,
+                                      "unit": "GB/s", "frac": gbps / HBM_PEAK_GBS, "algorithmic_bytes": nbytes,
+                                      "avg_ms": ms}),
         "cpu_baseline": cpu,
     }), flush=True)
 
