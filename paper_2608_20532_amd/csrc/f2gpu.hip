@@ -1017,8 +1017,15 @@ __device__ __forceinline__ void group_barrier(int* bar, int& epoch, int G, bool 
 __device__ __forceinline__ void put_dev(uint64_t* p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint64_t get_dev(const uint64_t* p) {
-    return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// device-scope (sc1) loads through a buffer resource: the same coherence as a
+// device-scope atomic load, but the compiler keeps many of them in flight
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t dev_rsrc(const uint64_t* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint64_t*>(base), 0, static_cast<int>(bytes), 0x00020000);
+}
+__device__ __forceinline__ uint64_t get_dev(__amdgpu_buffer_rsrc_t r, uint32_t word) {
+    const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(8 * word), 0, 16 /* sc1 */);
+    return (static_cast<uint64_t>(v.y) << 32) | v.x;
 }
 
 struct GroupRows {
@@ -1207,13 +1214,19 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
                     if (act) put_dev(mine + (kLgSlots * wave + k) * W + lane, acc[k]);
                 if (lane < 2 * kLgSlots) put_dev(mine + yi * W + fw + (lane & 1), yv);
                 group_barrier(bar, epoch, G, false);
+                // reads past a partial's rows land in another partial or past the
+                // resource (zero); their values are masked off
+                const __amdgpu_buffer_rsrc_t xr = dev_rsrc(X + (blk & 1) * G * xs, static_cast<uint32_t>(8 * G * xs));
                 for (int o = 0; o < G; ++o) {
                     if (o == g) continue;
-                    const uint64_t* other = X + ((blk & 1) * G + o) * xs;
+                    const uint32_t ob = static_cast<uint32_t>(o * xs);
+                    uint64_t v[kLgSlots];
 #pragma unroll
-                    for (int k = 0; k < kLgSlots; ++k)
-                        if (act) acc[k] ^= get_dev(other + (kLgSlots * wave + k) * W + lane);
-                    if (lane < 2 * kLgSlots) yv ^= get_dev(other + yi * W + fw + (lane & 1));
+                    for (int k = 0; k < kLgSlots; ++k) v[k] = get_dev(xr, ob + (kLgSlots * wave + k) * W + lane);
+                    const uint64_t vy = get_dev(xr, ob + yi * W + fw + (lane & 1));
+#pragma unroll
+                    for (int k = 0; k < kLgSlots; ++k) acc[k] ^= act ? v[k] : 0ull;
+                    yv ^= lane < 2 * kLgSlots ? vy : 0ull;
                 }
 #pragma unroll
                 for (int k = 0; k < kLgSlots; ++k) {  // + X, reloaded
@@ -1245,7 +1258,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
         }
         for (int ph = 0; ph < kLargeWaves; ++ph) {
             const int bq = ph & 1;
-            const int tb = 2 * kLgEnt * bq;  // this phase's two tables in tf (the reduce is done with it)
+            const int tb = kLgSlots * bq;  // this phase's published rows in tf (the reduce is done with it)
             if (wave == ph) {  // this wavefront's rows in order; earlier wavefronts' pivots already applied
                 unsigned newSlots = 0;
 #pragma unroll
@@ -1263,14 +1276,18 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
                         continue;
                     }
                     const int pw = p >> 6, pb = p & 63;
-                    uint64_t em = 0;
+                    // bit p of the wavefront's rows: gathered in every lane, read from lane pw
+                    uint32_t bits = 0;
 #pragma unroll
-                    for (int t = 0; t < kLgSlots; ++t) {
-                        if (t == s) continue;
-                        const bool hit = (readlane64(acc[t], pw) >> pb) & 1ull;
-                        acc[t] = xor_and(acc[t], hit ? ~0u : 0u, F);
-                        em |= hit ? (3ull << (2 * t)) : 0ull;
-                    }
+                    for (int t = 0; t < kLgSlots; ++t) bits |= static_cast<uint32_t>((acc[t] >> pb) & 1ull) << t;
+                    const uint32_t hits = __builtin_amdgcn_readlane(bits, pw) & ~(1u << s);
+#pragma unroll
+                    for (int t = 0; t < kLgSlots; ++t) acc[t] = xor_and(acc[t], ((hits >> t) & 1u) ? ~0u : 0u, F);
+                    uint32_t em = hits;  // slot t -> output-word lanes 2t, 2t+1
+                    em = (em | (em << 4)) & 0x0f0fu;
+                    em = (em | (em << 2)) & 0x3333u;
+                    em = (em | (em << 1)) & 0x5555u;
+                    em |= em << 1;
                     yv = xor_and(yv, lanes_of(em, lane), (lane & 1) ? Y1 : Y0);
                     newSlots |= 1u << s;
                     if (lane == 0) {
@@ -1278,37 +1295,21 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
                         atomicOr(reinterpret_cast<unsigned long long*>(&L.npm[pw]), 1ull << pb);
                     }
                 }
-                // the new rows, now fully reduced among themselves, as two 4-row tables
+                // publish the new rows, now fully reduced among themselves, in slot order
                 const int np = __popc(newSlots);
 #pragma unroll
                 for (int s = 0; s < kLgSlots; ++s) {
                     if (!((newSlots >> s) & 1u)) continue;
                     const int q = __popc(newSlots & ((1u << s) - 1u));
-                    const int e = tb + kLgEnt * (q >> 2) + (1 << (q & 3));
-                    L.tf[e][lane] = acc[s];
-                    if ((lane >> 1) == s) L.tz[e][lane & 1] = yv;
+                    L.tf[tb + q][lane] = acc[s];
+                    if ((lane >> 1) == s) L.tz[tb + q][lane & 1] = yv;
                     if (lane == 0) L.pubP[bq][q] = L.rowPiv[kLgSlots * ph + s];
-                }
-                wave_sync();
-#pragma unroll
-                for (int t = 0; t < 2; ++t) {
-                    GroupRows gr;
-                    gr.present = 0;
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const bool has = 4 * t + q < np;
-                        gr.present |= has ? (1u << q) : 0u;
-                        gr.f[q] = has ? L.tf[tb + kLgEnt * t + (1 << q)][lane] : 0ull;
-                        gr.z[q] = has ? L.tz[tb + kLgEnt * t + (1 << q)][lane & 1] : 0ull;
-                    }
-                    wave_sync();
-                    write_table(L, tb + kLgEnt * t, gr, lane, true);
                 }
                 if (lane == 0) L.pubN[bq] = np;
             }
             __syncthreads();
             const int np = L.pubN[bq];
-            if (wave != ph && np > 0) {  // the published rows: selection bits at their pivots, one entry per table
+            if (wave != ph && np > 0) {  // the published rows: selection bits at their pivots, then the rows
                 const int pk = lane < np ? L.pubP[bq][lane] : 0;
                 const int pkw = pk >> 6, pkb = pk & 63;
                 uint32_t sel[kLgSlots];
@@ -1319,17 +1320,13 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
                 for (int k = 0; k < kLgSlots; ++k)
                     sel[k] = static_cast<uint32_t>(__ballot(lane < np && ((wv[k] >> pkb) & 1ull)));
                 const uint32_t sy = spread_slots(sel, lane);
-                uint64_t t0[kLgSlots], t1[kLgSlots];
+                for (int q = 0; q < np; ++q) {
+                    const uint64_t Fv = L.tf[tb + q][lane];
+                    const uint64_t Zv = L.tz[tb + q][lane & 1];
 #pragma unroll
-                for (int k = 0; k < kLgSlots; ++k) {
-                    t0[k] = L.tf[tb + (sel[k] & 15u)][lane];
-                    t1[k] = L.tf[tb + kLgEnt + ((sel[k] >> 4) & 15u)][lane];
+                    for (int k = 0; k < kLgSlots; ++k) acc[k] = xor_and(acc[k], ((sel[k] >> q) & 1u) ? ~0u : 0u, Fv);
+                    yv = xor_and(yv, 0u - ((sy >> q) & 1u), Zv);
                 }
-                const uint64_t ty0 = L.tz[tb + (sy & 15u)][lane & 1];
-                const uint64_t ty1 = L.tz[tb + kLgEnt + ((sy >> 4) & 15u)][lane & 1];
-#pragma unroll
-                for (int k = 0; k < kLgSlots; ++k) acc[k] = xor3(acc[k], t0[k], t1[k]);
-                yv = xor3(yv, ty0, ty1);
             }
         }
         if (lane == 0 && ncon) {
