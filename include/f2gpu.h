@@ -116,10 +116,10 @@ typedef struct f2_model {
     uint32_t* ctx_flags;      /* [num_ctx] */
     int32_t* n_contra;        /* [num_ctx] */
     int64_t* first_contra_row;/* [num_ctx] */
-    int32_t max_n_bits;       /* host-side hint: the largest n of the batch, or -1 if not known.
-                                 Scheduling only: below 512 (every context within 8 feature words)
-                                 f2_fit_batch skips the cooperative launch that lets several
-                                 workgroups share one wide context; results never depend on it. */
+    int32_t max_n_bits;       /* -1, or an upper bound on the widths n of the batch, known on the
+                                 host: f2_fit_batch flags a wider context F2_CTX_BAD_WIDTH, and
+                                 below 512 (every context within 8 feature words) it does not
+                                 launch the wide-context kernel at all. */
 } f2_model;
 
 /*

@@ -123,7 +123,7 @@ __device__ __forceinline__ CtxDesc load_desc(const FitArgs& a, int64_t c) {
     ds.c = static_cast<int>(c);
     const int n = a.n_bits[c];
     ds.n = n;
-    if (n < 0 || n > F2_MAX_N_BITS) {
+    if (n < 0 || n > F2_MAX_N_BITS || (a.max_n >= 0 && n > a.max_n)) {  // outside the supported or declared range
         ds.bad = F2_CTX_BAD_WIDTH;
         return ds;
     }
@@ -649,7 +649,8 @@ __global__ __launch_bounds__(64 * kRegWaves) void k_fit_reg(FitArgs a) {
 // ---------------------------------------------------------------------------
 constexpr int kPivRec = kPivMaxFW + F2_Y_WORDS;  // record words
 constexpr int kPivCap = 64 * kPivMaxFW;          // d <= 512
-constexpr int kPivWaves = 8;
+constexpr int kPivWaves = 4;
+constexpr int kPivThreads = 64 * kPivWaves;
 
 template <int FW>
 __device__ __forceinline__ uint64_t sel_word(const uint64_t (&f)[FW], int wi) {
@@ -1635,49 +1636,43 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
     __syncthreads();
 }
 
-// contexts of classes 1-2 (fw <= 8 beyond the register kernel: pivot-indexed LDS
-// basis, kPivWaves wavefronts) and class 3 (fw > 8: large-context path) share one
-// launch: both run 8 wavefronts and are limited to one workgroup per compute
-// unit, so the union of their shared memory costs no occupancy
-union WideShared {
-    PivShared piv;
-    LargeShared large;
-};
-
-// Wide contexts first: with few of them (as many as a quarter of the workgroups
-// or fewer) each is fitted by a group of 4 workgroups, by 2 with up to half,
-// else by one.  Under a cooperative launch every workgroup is resident, which the
-// group barriers need; otherwise groups are single workgroups.  A group's
-// workgroups are blockIdx values congruent mod 8, which the dispatcher places on
-// one die (shared L2 for the exchange).
-__global__ __launch_bounds__(kLargeThreads) void k_fit_wide(FitArgs a) {
-    __shared__ WideShared U;
-    {
-        const int nl = a.plan[kClsLarge + 1] - a.plan[kClsLarge];
-        const int nwg = static_cast<int>(gridDim.x);
-        int G = 1;
-        if (a.coop && nwg % 32 == 0 && nwg / 4 <= kMaxGroups && 4 * nl <= nwg) G = 4;
-        else if (a.coop && nwg % 16 == 0 && nwg / 2 <= kMaxGroups && 2 * nl <= nwg) G = 2;
-        const int x = static_cast<int>(blockIdx.x), idx = x / 8;
-        const int g = idx % G, grp = (x % 8) + 8 * (idx / G), ngrp = nwg / G;
-        int epoch = 0;
-        for (int i = 0;; ++i) {
-            const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsLarge, i, -1, ngrp, grp));
-            if (c < 0) break;
-            fit_ctx_large(a, readlane_desc(load_desc(a, c), 0), U.large, G, g, a.plan + kBarHead + grp, epoch);
-        }
-    }
-    // classes 1 and 2 are adjacent in the plan: one list of LDS-basis contexts
+// contexts of classes 1-2 (fw <= 8 beyond the register kernel): pivot-indexed LDS
+// basis, kPivWaves wavefronts per workgroup, several workgroups per compute unit
+__global__ __launch_bounds__(kPivThreads) void k_fit_piv(FitArgs a) {
+    __shared__ PivShared S;
     for (int i = 0;; ++i) {
         const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsPiv, i, kClsPivLong));
         if (c < 0) break;
         const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
         switch (feat_words(ds.n)) {
-            case 1: fit_ctx_piv<1, kPivWaves>(a, ds, U.piv); break;
-            case 2: fit_ctx_piv<2, kPivWaves>(a, ds, U.piv); break;
-            case 3: case 4: fit_ctx_piv<4, kPivWaves>(a, ds, U.piv); break;
-            default: fit_ctx_piv<8, kPivWaves>(a, ds, U.piv); break;
+            case 1: fit_ctx_piv<1, kPivWaves>(a, ds, S); break;
+            case 2: fit_ctx_piv<2, kPivWaves>(a, ds, S); break;
+            case 3: case 4: fit_ctx_piv<4, kPivWaves>(a, ds, S); break;
+            default: fit_ctx_piv<8, kPivWaves>(a, ds, S); break;
         }
+    }
+}
+
+// Wide contexts (class 3): with few of them (as many as a quarter of the
+// workgroups or fewer) each is fitted by a group of 4 workgroups, by 2 with up to
+// half, else by one.  Under a cooperative launch every workgroup is resident,
+// which the group barriers need; otherwise groups are single workgroups.  A
+// group's workgroups are blockIdx values congruent mod 8, which the dispatcher
+// places on one die (shared L2 for the exchange).
+__global__ __launch_bounds__(kLargeThreads) void k_fit_wide(FitArgs a) {
+    __shared__ LargeShared U;
+    const int nl = a.plan[kClsLarge + 1] - a.plan[kClsLarge];
+    const int nwg = static_cast<int>(gridDim.x);
+    int G = 1;
+    if (a.coop && nwg % 32 == 0 && nwg / 4 <= kMaxGroups && 4 * nl <= nwg) G = 4;
+    else if (a.coop && nwg % 16 == 0 && nwg / 2 <= kMaxGroups && 2 * nl <= nwg) G = 2;
+    const int x = static_cast<int>(blockIdx.x), idx = x / 8;
+    const int g = idx % G, grp = (x % 8) + 8 * (idx / G), ngrp = nwg / G;
+    int epoch = 0;
+    for (int i = 0;; ++i) {
+        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsLarge, i, -1, ngrp, grp));
+        if (c < 0) break;
+        fit_ctx_large(a, readlane_desc(load_desc(a, c), 0), U, G, g, a.plan + kBarHead + grp, epoch);
     }
 }
 
@@ -2353,15 +2348,18 @@ int wide_resident_workgroups() {
 // the fit: plan (two kernels), then the class kernels.  The wide kernel runs one
 // workgroup per compute unit as a cooperative launch (so that a group of
 // workgroups can fit one context together), else a plain launch of up to 256.
+constexpr int kPivGrid = 768;  // LDS-basis workgroups: three per compute unit (LDS-bound)
 void launch_fit(FitArgs a, hipStream_t s) {
     const int32_t C = a.num_ctx;
     const int plan_blocks = static_cast<int>((static_cast<int64_t>(C) + kPlanThreads - 1) / kPlanThreads);
     hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
     hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
     hipLaunchKernelGGL(k_fit_reg, dim3(fit_grid((C + kRegWaves - 1) / kRegWaves, 256)), dim3(64 * kRegWaves), 0, s, a);
-    // a batch known to hold no context wider than 8 feature words gains nothing
-    // from the cooperative launch (which costs tens of microseconds of setup)
-    const int res = (a.max_n >= 0 && a.max_n < 512) ? 0 : wide_resident_workgroups();
+    hipLaunchKernelGGL(k_fit_piv, dim3(fit_grid(C, kPivGrid)), dim3(kPivThreads), 0, s, a);
+    // a batch whose declared widths stay below 512 holds no wide context (wider
+    // ones are rejected by the plan), so the wide kernel is not launched at all
+    if (a.max_n >= 0 && a.max_n < 512) return;
+    const int res = wide_resident_workgroups();
     if (res >= 32) {
         a.coop = 1;
         void* args[] = {&a};

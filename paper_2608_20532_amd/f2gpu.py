@@ -125,11 +125,13 @@ def f2_encode_workspace_bytes(model: "Model", num_queries: int) -> int:
 class Model:
     """Device buffers of a fitted model (the f2_model struct), allocated with torch."""
 
-    def __init__(self, n_bits_host, device="cuda"):
+    def __init__(self, n_bits_host, device="cuda", max_n_bits=None):
         import torch
         n_bits_host = np.ascontiguousarray(n_bits_host, np.int32)
         self.num_ctx = len(n_bits_host)
         self.n_bits_host = n_bits_host
+        # declared width bound (f2_model.max_n_bits): the largest width by default
+        self.max_n_bits = (int(n_bits_host.max()) if self.num_ctx else 0) if max_n_bits is None else int(max_n_bits)
         bo, po, mo = f2_fit_layout(n_bits_host)
         self.basis_off_host, self.piv_off_host, self.map_off_host = bo, po, mo
         dev = torch.device(device)
@@ -156,7 +158,7 @@ class Model:
                 _ptr(self.basis), _ptr(self.pivots), _ptr(self.maps), _ptr(self.tables), _ptr(self.rank),
                 _ptr(self.ctx_flags),
                 _ptr(self.n_contra), _ptr(self.first_contra_row),
-                int(self.n_bits_host.max()) if self.num_ctx else 0)
+                self.max_n_bits)
         return self._struct
 
 

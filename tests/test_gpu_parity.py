@@ -207,6 +207,36 @@ def test_fit_bad_segments_and_widths(f2):
     assert parity.host(model2.ctx_flags, np.uint32)[5] == oracle.CTX_BAD_OUTPUT
 
 
+def test_fit_declared_width_bound(f2):
+    """max_n_bits is a contract: a context wider than the declared bound is flagged
+    F2_CTX_BAD_WIDTH with rank 0 and the others fit as usual, whether the bound lets
+    the wide-context kernel launch or not."""
+    import torch
+    from paper_2608_20532_amd import f2gpu
+    widths = [40, 100, 700, 63, 200, 511, 512]
+    wl = _random_batch(5, widths)
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    rows_d, off_d = parity.to_dev(wl.rows), parity.to_dev(wl.row_off)
+    for bound in (99, 511, 700, -1):
+        print(f"declared width bound {bound}", flush=True)
+        model = f2gpu.Model(wl.n_bits, max_n_bits=bound)
+        nb = f2gpu.f2_fit_workspace_bytes(model.num_ctx)
+        ws = f2gpu.workspace(nb)
+        assert f2gpu.f2_fit_batch(rows_d, wl.rows.size, off_d, model, ws, nb) == 0
+        torch.cuda.synchronize()
+        g = parity.model_to_host(model)
+        over = (wl.n_bits > bound) if bound >= 0 else np.zeros(len(widths), bool)
+        assert (g["flags"][over] == oracle.CTX_BAD_WIDTH).all() and not g["rank"][over].any()
+        ok = ~over
+        for k, r in (("flags", ref.flags), ("rank", ref.rank), ("n_contra", ref.n_contra), ("first", ref.first_contra)):
+            assert np.array_equal(g[k][ok], r[ok]), k
+        for c in np.nonzero(ok)[0]:
+            d, W, r = int(wl.n_bits[c]) + 1, (int(wl.n_bits[c]) + 64) // 64 + 2, int(ref.rank[c])
+            mo, bo = int(ref.map_off[c]), int(ref.basis_off[c])
+            assert np.array_equal(g["maps"][mo:mo + 2 * d], ref.maps[mo:mo + 2 * d]), f"maps of context {c}"
+            assert np.array_equal(g["basis"][bo:bo + r * W], ref.basis[bo:bo + r * W]), f"basis of context {c}"
+
+
 def test_fit_host_errors(f2):
     from paper_2608_20532_amd import f2gpu
     wl = synth.fit_workload(1)
