@@ -62,7 +62,7 @@ typedef enum {
 enum {
     F2_CTX_CONTRADICTION = 1u, /* n_contra > 0: some row had a zero-feature, nonzero-output residual */
     F2_CTX_BAD_SEGMENT = 2u,   /* row segment negative, past rows_words, or not a multiple of fw+2 words */
-    F2_CTX_BAD_WIDTH = 4u,     /* n_bits outside [0, F2_MAX_N_BITS] */
+    F2_CTX_BAD_WIDTH = 4u,     /* n_bits outside [0, F2_MAX_N_BITS], or above a declared max_n_bits */
     F2_CTX_BAD_OUTPUT = 8u     /* output offsets of this context fall outside the output buffers */
 };
 

@@ -342,7 +342,7 @@ def test_encode_grouped_path_random_widths(f2):
     ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
     model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
     stride = 3
-    nq = 150_000
+    nq = 200_000   # grouped from 196,608 queries (and 4 per context) on
     ctx = rng.integers(-3, wl.num_ctx + 3, size=nq).astype(np.int32)
     x = np.zeros((nq, stride), np.uint64)
     ok = (ctx >= 0) & (ctx < wl.num_ctx)
@@ -390,7 +390,7 @@ def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
     nb = f2.f2_fit_workspace_bytes(model.num_ctx)
     ws = f2.workspace(nb)
     assert f2.f2_fit_batch(parity.to_dev(wl.rows), wl.rows.size, parity.to_dev(row_off), model, ws, nb) == 0
-    nq, stride = 100_000, 2
+    nq, stride = 240_000, 2   # the whole batch is grouped (196,608 queries or more), its halves are not
     ctx, x, _ = synth.queries(wl, nq, stride, 0.05, 0.0)
     rng = np.random.default_rng(41)
     idx = rng.choice(nq, size=3000, replace=False)
