@@ -663,9 +663,10 @@ __device__ __forceinline__ uint64_t sel_word(const uint64_t (&f)[FW], int wi) {
 
 struct PivShared {
     uint64_t rec[kPivCap][kPivRec];
-    uint64_t pm[kPivMaxFW];
+    uint64_t pm[kPivMaxFW];   // pivot columns of the retained rows
+    uint64_t npm[kPivMaxFW];  // pivot columns of the rows the current round added
     int flag[kPivWaves];
-    int contra;
+    int contra, nnew;
     long long first, round_first;
 };
 
@@ -705,16 +706,27 @@ __device__ __forceinline__ void piv_reduce(PivShared& S, int fw, uint64_t (&f)[F
     }
 }
 
-// insertion loop of one block (one wavefront); returns the rank after the block
+// in-block elimination of one wavefront's block, in registers: the earliest row
+// with a nonzero feature residual becomes a new basis row and stays in its lane;
+// its pivot is cleared from every other row of the block, earlier new rows
+// included, so the new rows end fully reduced among themselves (and hold no
+// retained pivot: the block was reduced first).  Rows before it with a zero
+// residual are classified on the way.  The new rows then go to their records,
+// their pivots to npm and their count to nnew; the retained rows are cleared of
+// the new pivots afterwards by all wavefronts (piv_backsub).
 template <int FW>
-__device__ int piv_insert(PivShared& S, int n, int d, int fw, int rank, int64_t b0, bool valid, uint64_t (&f)[FW],
-                          uint64_t& y0, uint64_t& y1, int& ncon, long long& firstc) {
+__device__ void piv_insert(PivShared& S, int n, int64_t b0, bool valid, uint64_t (&f)[FW], uint64_t& y0, uint64_t& y1,
+                           int& ncon, long long& firstc) {
     const int lane = threadIdx.x & 63;
     const int cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
     uint64_t pending = __ballot(valid);
+    uint64_t ins = 0;  // lanes holding new basis rows
+    uint64_t npm[FW];  // their pivot columns
+#pragma unroll
+    for (int w = 0; w < FW; ++w) npm[w] = 0;
+    int mypiv = 0;  // this lane's pivot, where it holds a new basis row
     while (pending) {
-        __builtin_amdgcn_wave_barrier();
         uint64_t any = f[0];
 #pragma unroll
         for (int w = 1; w < FW; ++w) any |= f[w];
@@ -742,38 +754,62 @@ __device__ int piv_insert(PivShared& S, int n, int d, int fw, int rank, int64_t 
         }
         if (p < 0) p = n;
         const int pw = p >> 6, pb = p & 63;
-        {  // rows of the block that hold bit p
-            const uint32_t mm = bit_mask(sel_word<FW>(f, pw), pb);
+        const uint32_t mm = bit_mask(sel_word<FW>(f, pw), pb) & (lane == j ? 0u : ~0u);
 #pragma unroll
-            for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, F[w]);
-            y0 = xor_and(y0, mm, Y0);
-            y1 = xor_and(y1, mm, Y1);
-        }
-        // clear p from every retained row (record s for each set pivot bit s)
-        for (int s = lane; s < d; s += 64) {
-            if (!((S.pm[s >> 6] >> (s & 63)) & 1ull)) continue;
-            uint64_t* rec = S.rec[s];
-            if ((rec[pw] >> pb) & 1ull) {
+        for (int w = 0; w < FW; ++w) f[w] = xor_and(f[w], mm, F[w]);
+        y0 = xor_and(y0, mm, Y0);
+        y1 = xor_and(y1, mm, Y1);
+        if (lane == j) mypiv = p;
 #pragma unroll
-                for (int w = 0; w < FW; ++w) rec[w] ^= F[w];
-                rec[FW] ^= Y0;
-                rec[FW + 1] ^= Y1;
-            }
-        }
-        __builtin_amdgcn_wave_barrier();
-        if (lane == 0) {
-            uint64_t* rec = S.rec[p];
-#pragma unroll
-            for (int w = 0; w < FW; ++w) rec[w] = F[w];
-            rec[FW] = Y0;
-            rec[FW + 1] = Y1;
-            S.pm[pw] |= 1ull << pb;
-        }
-        ++rank;
+        for (int w = 0; w < FW; ++w)
+            if (w == pw) npm[w] |= 1ull << pb;
+        ins |= 1ull << j;
         pending &= ~(1ull << j);
     }
-    (void)fw;
-    return rank;
+    if ((ins >> lane) & 1ull) {
+        uint64_t* rec = S.rec[mypiv];
+#pragma unroll
+        for (int w = 0; w < FW; ++w) rec[w] = f[w];
+        rec[FW] = y0;
+        rec[FW + 1] = y1;
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int w = 0; w < FW; ++w) S.npm[w] = npm[w];
+        S.nnew = __popcll(ins);
+    }
+}
+
+// clear the round's new pivots from the retained rows (records of S.pm), one
+// record per thread.  The new rows hold no other new pivot, so a record's bits
+// at the new pivots, read once before any addition, select the rows to add.
+template <int FW, int NW>
+__device__ __forceinline__ void piv_backsub(PivShared& S, int d, int fw) {
+    for (int s = threadIdx.x; s < d; s += 64 * NW) {
+        if (!((S.pm[s >> 6] >> (s & 63)) & 1ull)) continue;
+        uint64_t* rec = S.rec[s];
+        uint64_t R[FW + 2];
+#pragma unroll
+        for (int w = 0; w < FW + 2; ++w) R[w] = rec[w];
+        uint64_t R0[FW];
+#pragma unroll
+        for (int w = 0; w < FW; ++w) R0[w] = R[w];
+#pragma unroll
+        for (int w = 0; w < FW; ++w) {
+            if (w >= fw) break;
+            uint64_t m = S.npm[w];
+            while (m) {
+                const int b = ffs64(m);
+                m &= m - 1;
+                const uint32_t mk = bit_mask(R0[w], b);
+                const uint64_t* nr = S.rec[64 * w + b];
+#pragma unroll
+                for (int u = 0; u < FW + 2; ++u) R[u] = xor_and(R[u], mk, nr[u]);
+            }
+        }
+#pragma unroll
+        for (int w = 0; w < FW + 2; ++w) rec[w] = R[w];
+    }
 }
 
 template <int FW, int NW>
@@ -786,9 +822,14 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
     const uint64_t* R = a.rows + ds.row0;
     const uint64_t tmask = top_mask(n, fw);
 
-    if (tid < kPivMaxFW) S.pm[tid] = 0;
+    static_assert(NW > 1, "rounds of several wavefronts");
+    if (tid < kPivMaxFW) {
+        S.pm[tid] = 0;
+        S.npm[tid] = 0;
+    }
     if (tid == 0) {
         S.contra = 0;
+        S.nnew = 0;
         S.first = -1;
     }
     __syncthreads();
@@ -817,17 +858,12 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
 #pragma unroll
         for (int w = 1; w < FW; ++w) any |= f[w];
         const bool has_nz = __ballot(valid && any != 0) != 0;
-        int wstar;
-        if constexpr (NW > 1) {
-            if (lane == 0) S.flag[wave] = has_nz ? 1 : 0;
-            if (tid == 0) S.round_first = 0x7fffffffffffffffll;
-            __syncthreads();
-            wstar = NW;
-            for (int w = NW - 1; w >= 0; --w)
-                if (S.flag[w]) wstar = w;
-        } else {
-            wstar = has_nz ? 0 : 1;
-        }
+        if (lane == 0) S.flag[wave] = has_nz ? 1 : 0;
+        if (tid == 0) S.round_first = 0x7fffffffffffffffll;
+        __syncthreads();
+        int wstar = NW;
+        for (int w = NW - 1; w >= 0; --w)
+            if (S.flag[w]) wstar = w;
         int ncon = 0;
         long long firstc = -1;
         if (wave < wstar) {  // every residual is zero: redundant or contradictory rows
@@ -837,23 +873,24 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
                 firstc = bw + ffs64(cm);
             }
         } else if (wave == wstar) {
-            rank = piv_insert<FW>(S, n, d, fw, rank, bw, valid, f, y0, y1, ncon, firstc);
+            piv_insert<FW>(S, n, bw, valid, f, y0, y1, ncon, firstc);
         }
         if (lane == 0 && ncon) {
             atomicAdd(&S.contra, ncon);
-            if constexpr (NW > 1) atomicMin(&S.round_first, firstc);
-            else S.round_first = firstc;
+            atomicMin(&S.round_first, firstc);
         }
-        if constexpr (NW > 1) {
+        __syncthreads();
+        if (S.nnew) {  // retained rows lose the new pivots, then the new rows join them
+            piv_backsub<FW, NW>(S, d, fw);
             __syncthreads();
-            if (tid == 0 && S.first < 0 && S.round_first != 0x7fffffffffffffffll) S.first = S.round_first;
-            rank = 0;
-            for (int w = 0; w < fw; ++w) rank += __popcll(S.pm[w]);
+            if (tid < fw) S.pm[tid] |= S.npm[tid];
             __syncthreads();
-        } else {
-            if (lane == 0 && ncon && S.first < 0) S.first = firstc;
-            __builtin_amdgcn_wave_barrier();
         }
+        if (tid == 0 && S.first < 0 && S.round_first != 0x7fffffffffffffffll) S.first = S.round_first;
+        rank = 0;
+        for (int w = 0; w < fw; ++w) rank += __popcll(S.pm[w]);
+        __syncthreads();
+        if (tid == 0) S.nnew = 0;
         b0 += 64 * static_cast<int64_t>(wstar < NW ? wstar + 1 : NW);
     }
     __syncthreads();
