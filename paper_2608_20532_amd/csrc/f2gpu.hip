@@ -182,13 +182,16 @@ __device__ void write_bad_context(const FitArgs& a, const CtxDesc& ds) {
 // a counting sort over (class, cost bucket) bins in two kernels (per-block
 // histograms; a scatter that scans them) with no device-wide atomics: on a chip
 // of eight dies those serialise far from the compute units.
-// Workspace (int32): [0, 5) list offsets per class, [16, 16 + C) the lists,
-// then C sort keys and a kPlanBins histogram per plan block.
+// Workspace (int32): [0, 5) list offsets per class, [kPivNext] the work counter
+// of the LDS-basis kernel, [kBarHead, kPlanHead) barrier counters of workgroup
+// groups, [kPlanHead, kPlanHead + C) the lists, then C sort keys and a
+// kPlanBins histogram per plan block.
 // ---------------------------------------------------------------------------
 constexpr int kRegMaxFW = 3;
 constexpr int kPivMaxFW = 8;
 constexpr int kLongRows = 256;  // contexts with more rows take the multi-wavefront kernel
 enum { kClsReg = 0, kClsPiv = 1, kClsPivLong = 2, kClsLarge = 3, kNumCls = 4 };
+constexpr int kPivNext = 8;                 // plan word: next list position for the LDS-basis kernel
 constexpr int kBarHead = 16;                // plan words kBarHead ..: barrier counters of workgroup groups
 constexpr int kMaxGroups = 128;
 constexpr int kPlanHead = kBarHead + kMaxGroups;
@@ -239,6 +242,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_count(FitArgs a) {
     sBin[tid] = 0;
     __syncthreads();
     if (blockIdx.x == 0 && tid < kMaxGroups) a.plan[kBarHead + tid] = 0;
+    if (blockIdx.x == 0 && tid == 0) a.plan[kPivNext] = 0;
     const int64_t c = static_cast<int64_t>(blockIdx.x) * kPlanThreads + tid;
     if (c < a.num_ctx) {
         const CtxDesc ds = load_desc(a, c);
@@ -265,7 +269,18 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_scatter(FitArgs a, int bl
     const int tid = threadIdx.x, lane = tid & 63;
     const int g0 = static_cast<int>(blockIdx.x);
     int total = 0, before = 0;
-    for (int g = 0; g < blocks; ++g) {
+    int g = 0;
+    for (; g + 8 <= blocks; g += 8) {  // eight loads in flight
+        int v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = P.hist[static_cast<int64_t>(g + k) * kPlanBins + tid];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            before += g + k < g0 ? v[k] : 0;
+            total += v[k];
+        }
+    }
+    for (; g < blocks; ++g) {
         const int v = P.hist[static_cast<int64_t>(g) * kPlanBins + tid];
         before += g < g0 ? v : 0;
         total += v;
@@ -1675,12 +1690,18 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
 }
 
 // contexts of classes 1-2 (fw <= 8 beyond the register kernel): pivot-indexed LDS
-// basis, kPivWaves wavefronts per workgroup, several workgroups per compute unit
+// basis, kPivWaves wavefronts per workgroup, several workgroups per compute unit.
+// The list (largest first) is taken greedily: workgroup g starts at position g,
+// then each takes the next free position from a counter as it finishes one (the
+// fetch is issued when a context starts, so its latency hides behind the work).
 __global__ __launch_bounds__(kPivThreads) void k_fit_piv(FitArgs a) {
     __shared__ PivShared S;
-    for (int i = 0;; ++i) {
-        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsPiv, i, kClsPivLong));
-        if (c < 0) break;
+    __shared__ int sNext;
+    const int lo = a.plan[kClsPiv], cnt = a.plan[kClsPivLong + 1] - lo;
+    for (int i = static_cast<int>(blockIdx.x); i < cnt;) {
+        const int c = __builtin_amdgcn_readfirstlane(a.plan[kPlanHead + lo + i]);
+        int next = 0;
+        if (threadIdx.x == 0) next = atomicAdd(&a.plan[kPivNext], 1) + static_cast<int>(gridDim.x);
         const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
         switch (feat_words(ds.n)) {
             case 1: fit_ctx_piv<1, kPivWaves>(a, ds, S); break;
@@ -1688,6 +1709,10 @@ __global__ __launch_bounds__(kPivThreads) void k_fit_piv(FitArgs a) {
             case 3: case 4: fit_ctx_piv<4, kPivWaves>(a, ds, S); break;
             default: fit_ctx_piv<8, kPivWaves>(a, ds, S); break;
         }
+        if (threadIdx.x == 0) sNext = next;
+        __syncthreads();
+        i = sNext;
+        __syncthreads();
     }
 }
 
