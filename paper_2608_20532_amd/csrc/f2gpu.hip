@@ -2106,13 +2106,204 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_scatter(EncArgs e, SortArg
     }
 }
 
+// In grouped order the lanes of a wavefront mostly share one context.  Such a
+// context's map columns and parity-check rows (or, with few basis rows, its
+// basis rows and pivots) are staged in LDS by the whole wavefront with coalesced
+// loads, and each lane masks the broadcast columns with its own phi bits: one
+// sign-extended bit per column, where the per-lane path gathers a column per
+// set bit with divergent addresses.  Staging capacity: contexts of up to 4
+// feature words (d <= 256); wider ones take the per-lane path.
+constexpr int kEncStageCols = 256;                // map columns (16 B each), words [0, 512)
+constexpr int kEncStageRows = 2 * kEncStageCols;  // first word of the parity-check rows (<= 128 x 4 words)
+constexpr int kEncStageWords = 4 * kEncStageCols; // words of one wavefront's stage (8 KB)
+struct EncStage {
+    uint64_t w[kEncThreads / 64][kEncStageWords];
+};
+
+// the staged context's geometry (uniform)
+struct StageCtx {
+    int n, d, fw, r;
+    bool rows;  // parity-check rows (else: basis rows)
+};
+
+// whole wavefront: stage context c (valid, fw <= 4) in the wavefront's LDS area
+__device__ __forceinline__ StageCtx stage_context(const EncArgs& e, int c, uint64_t* st) {
+    const int lane = threadIdx.x & 63;
+    StageCtx g;
+    g.n = e.n_bits[c];
+    g.d = g.n + 1;
+    g.fw = feat_words(g.n);
+    const int r0 = e.rank[c];
+    g.r = r0 < 0 ? 0 : (r0 > g.d ? g.d : r0);
+    g.rows = has_parity_rows(g.d, g.r);
+    if (g.rows) {  // columns at words [0, 2d), the t fw words of parity-check rows at kEncStageRows
+        const uint64_t* M = e.maps + e.map_off[c];
+        const uint64_t* H = e.tables + e.basis_off[c];
+        const int t = g.d - g.r;
+        for (int k = lane; k < 2 * g.d; k += 64) st[k] = M[k];
+        for (int k = lane; k < t * g.fw; k += 64) st[kEncStageRows + k] = H[k];
+    } else {  // basis rows (r (fw + 2) words, r < d / 2 <= 128), then the pivots as words
+        const uint64_t* B = e.basis + e.basis_off[c];
+        const int32_t* P = e.pivots + e.piv_off[c];
+        const int nw = g.r * (g.fw + F2_Y_WORDS);
+        for (int k = lane; k < nw; k += 64) st[k] = B[k];
+        for (int k = lane; k < g.r; k += 64) st[nw + k] = static_cast<uint64_t>(P[k]);
+    }
+    wave_sync();
+    return g;
+}
+
+template <int FW>
+__device__ __forceinline__ bool encode_staged(const EncArgs& e, const StageCtx& g, const uint64_t* st,
+                                              const uint64_t* xq, uint64_t& z0, uint64_t& z1) {
+    const int S = e.stride, n = g.n, d = g.d, fw = g.fw, cw = n >> 6;
+    const uint64_t cbit = 1ull << (n & 63);
+    uint64_t xv[4] = {0, 0, 0, 0};
+    if (S == 2 || S == 4) {  // 16-byte loads (a query's words start 16-byte aligned)
+        const uint4* x4 = reinterpret_cast<const uint4*>(xq);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            if (k >= S / 2) break;
+            const uint4 v = x4[k];
+            xv[2 * k] = (static_cast<uint64_t>(v.y) << 32) | v.x;
+            xv[2 * k + 1] = (static_cast<uint64_t>(v.w) << 32) | v.z;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (k < S) xv[k] = xq[k];
+    }
+    bool outside = false;  // x bits at or above n
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        if (w >= S) break;
+        if (w > cw) outside |= xv[w] != 0;
+        else if (w == cw) outside |= (xv[w] >> (n & 63)) != 0;
+    }
+    for (int w = 4; w < S; ++w) outside |= xq[w] != 0;  // fw <= 4: words past the fourth are outside
+    uint64_t ph[FW];
+#pragma unroll
+    for (int w = 0; w < FW; ++w) ph[w] = (w < fw ? xv[w] : 0ull) | (w == cw ? cbit : 0ull);
+    if (g.rows) {
+        // T(phi): every staged column, masked by its bit of phi (the columns past
+        // n hold stale words, and their mask is zero)
+        const uint4* col = reinterpret_cast<const uint4*>(st);
+        uint32_t a0 = 0, a1 = 0, a2 = 0, a3 = 0;
+#pragma unroll
+        for (int w = 0; w < FW; ++w) {
+            if (w >= fw) break;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const uint32_t half = h ? static_cast<uint32_t>(ph[w] >> 32) : static_cast<uint32_t>(ph[w]);
+                const int j0 = 64 * w + 32 * h;
+                if (j0 >= d) break;
+#pragma unroll
+                for (int u0 = 0; u0 < 32; u0 += 8) {
+                    if (j0 + u0 >= d) break;
+#pragma unroll
+                    for (int u = u0; u < u0 + 8; ++u) {
+                        const uint4 v = col[j0 + u];
+                        const uint32_t mk = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(half), u, 1));
+                        a0 = __builtin_amdgcn_bitop3_b32(a0, mk, v.x, 0x78);
+                        a1 = __builtin_amdgcn_bitop3_b32(a1, mk, v.y, 0x78);
+                        a2 = __builtin_amdgcn_bitop3_b32(a2, mk, v.z, 0x78);
+                        a3 = __builtin_amdgcn_bitop3_b32(a3, mk, v.w, 0x78);
+                    }
+                }
+            }
+        }
+        z0 = (static_cast<uint64_t>(a1) << 32) | a0;
+        z1 = (static_cast<uint64_t>(a3) << 32) | a2;
+        // support: even overlap with every parity-check row
+        const uint64_t* H = st + kEncStageRows;
+        const int t = d - g.r;
+        uint32_t odd = 0;
+        for (int f = 0; f < t; ++f) {
+            uint64_t acc = 0;
+#pragma unroll
+            for (int w = 0; w < FW; ++w)
+                if (w < fw) acc ^= H[f * fw + w] & ph[w];
+            odd |= static_cast<uint32_t>(__popcll(acc));
+        }
+        return (odd & 1u) == 0 && !outside;
+    }
+    // few basis rows: the rows whose pivot bit phi holds sum to [phi | T(phi)]
+    // exactly when phi is in the span
+    const int W = fw + F2_Y_WORDS;
+    const uint64_t* piv = st + g.r * W;
+    uint64_t acc[FW];
+#pragma unroll
+    for (int w = 0; w < FW; ++w) acc[w] = 0;
+    uint64_t y0 = 0, y1 = 0;
+    for (int k = 0; k < g.r; ++k) {
+        const int p = static_cast<int>(piv[k]);
+        uint64_t pwd = ph[0];
+#pragma unroll
+        for (int w = 1; w < FW; ++w) pwd = (p >> 6) == w ? ph[w] : pwd;
+        const uint32_t mk = bit_mask(pwd, p & 63);
+        const uint64_t* row = st + k * W;
+#pragma unroll
+        for (int w = 0; w < FW; ++w)
+            if (w < fw) acc[w] = xor_and(acc[w], mk, row[w]);
+        y0 = xor_and(y0, mk, row[fw]);
+        y1 = xor_and(y1, mk, row[fw + 1]);
+    }
+    uint64_t diff = 0;
+#pragma unroll
+    for (int w = 0; w < FW; ++w) diff |= acc[w] ^ ph[w];
+    z0 = y0;
+    z1 = y1;
+    return diff == 0 && !outside;
+}
+
+constexpr int kSharedCtxPerWave = 4;  // contexts of a wavefront taken through the stage
+
 __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortArgs s) {
+    __shared__ EncStage sStage;
     const int64_t i = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
-    if (i >= e.nq) return;
-    const int2 qc = s.perm[i];
+    const bool live = i < e.nq;
+    const int2 qc = live ? s.perm[i] : make_int2(0, 0);
+    uint64_t* st = sStage.w[threadIdx.x >> 6];
     Word2 out, fl;
-    fl.x = encode_one(e, qc.y, qc.x, out.x, out.y);
-    fl.y = 0;
+    out.x = out.y = 0;
+    fl.x = fl.y = 0;
+    bool done = !live;
+    // with one context per bin the grouped order is exact and a wavefront holds
+    // one or two contexts; wider bins interleave their contexts' queries, and the
+    // per-lane path serves them better
+    const int nshared = s.bin_shift == 0 ? kSharedCtxPerWave : 0;
+    for (int k = 0; k < nshared; ++k) {  // the wavefront's contexts, first lane's first
+        const uint64_t todo = __ballot(!done);
+        if (!todo) break;
+        const int c0 = __builtin_amdgcn_readlane(qc.y, ffs64(todo));
+        if (c0 < 0 || c0 >= e.num_ctx || (e.ctx_flags[c0] & kBadCtx)) {
+            if (!done && qc.y == c0) {
+                fl.x = F2_Q_BAD_CTX;
+                done = true;
+            }
+            continue;
+        }
+        if (feat_words(e.n_bits[c0]) > 4) break;  // wide: per-lane path
+        const StageCtx g = stage_context(e, c0, st);
+        if (!done && qc.y == c0) {
+            fl.x = (e.ctx_flags[c0] & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0;
+            const uint64_t* xq = e.x + static_cast<int64_t>(qc.x) * e.stride;
+            bool in;
+            switch (g.fw) {
+                case 1: in = encode_staged<1>(e, g, st, xq, out.x, out.y); break;
+                case 2: in = encode_staged<2>(e, g, st, xq, out.x, out.y); break;
+                default: in = encode_staged<4>(e, g, st, xq, out.x, out.y); break;
+            }
+            if (!in) {
+                fl.x |= F2_Q_OUT_OF_SPAN;
+                out.x = out.y = 0;
+            }
+            done = true;
+        }
+        wave_sync();  // the stage is rewritten for the next context
+    }
+    if (!done) fl.x = encode_one(e, qc.y, qc.x, out.x, out.y);  // lanes of further contexts
+    if (!live) return;
     if (s.direct) {
         *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
         e.qflags[qc.x] = static_cast<uint8_t>(fl.x);
