@@ -848,26 +848,49 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
         S.first = -1;
     }
     __syncthreads();
+    // the next round's block is loaded while this round runs, on the guess that
+    // the round completes all NW blocks (it does once the basis stops growing);
+    // not for the widest records, whose registers it would cost occupancy
+    constexpr bool kPrefetch = FW <= 4;
+    // raw words of this wavefront's row in the block at base, row index clamped
+    // into the segment (lanes past its end are masked at use).  Up to 4 feature
+    // words every load is issued (fw >= FW - 1 there, so word FW - 1 is still in
+    // the row): a fixed count of loads in flight, which the wait for them can count.
+    auto load_raw = [&](int64_t base, uint64_t (&raw)[FW + 2]) {
+        const int64_t ii = base + 64 * wave + lane;
+        const uint64_t* row = R + (ii < m ? ii : m - 1) * Wr;
+#pragma unroll
+        for (int w = 0; w < FW; ++w) raw[w] = (kPrefetch || w < fw) ? row[w] : 0ull;
+        raw[FW] = row[fw];
+        raw[FW + 1] = row[fw + 1];
+    };
+    uint64_t pre[FW + 2];
+    int64_t pre_b0 = -1;
     int rank = 0;
     int64_t b0 = 0;
     while (b0 < m) {
         const int64_t bw = b0 + 64 * wave;  // this wavefront's block
         const int64_t i = bw + lane;
         const bool valid = i < m;
-        uint64_t f[FW], y0 = 0, y1 = 0;
+        uint64_t raw[FW + 2];
+        if (kPrefetch && pre_b0 == b0) {
 #pragma unroll
-        for (int w = 0; w < FW; ++w) f[w] = 0;
-        if (valid) {  // rows have fw + 2 words (fw <= FW)
-            const uint64_t* row = R + i * Wr;
-#pragma unroll
-            for (int w = 0; w < FW; ++w)
-                if (w < fw) f[w] = row[w];
-            y0 = row[fw];
-            y1 = row[fw + 1];
-#pragma unroll
-            for (int w = 0; w < FW; ++w)
-                if (w == fw - 1) f[w] &= tmask;
+            for (int w = 0; w < FW + 2; ++w) raw[w] = pre[w];
+        } else {
+            load_raw(b0, raw);
         }
+        if constexpr (kPrefetch) {  // issued unconditionally (a block past the end reads the last row)
+            pre_b0 = b0 + 64 * NW;
+            load_raw(pre_b0, pre);
+        }
+        uint64_t f[FW], y0, y1;
+#pragma unroll
+        for (int w = 0; w < FW; ++w) f[w] = (valid && w < fw) ? raw[w] : 0ull;
+#pragma unroll
+        for (int w = 0; w < FW; ++w)
+            if (w == fw - 1) f[w] &= tmask;
+        y0 = valid ? raw[FW] : 0ull;
+        y1 = valid ? raw[FW + 1] : 0ull;
         if (rank > 0) piv_reduce<FW>(S, fw, f, y0, y1);
         uint64_t any = f[0];
 #pragma unroll
