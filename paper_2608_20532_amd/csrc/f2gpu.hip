@@ -77,6 +77,7 @@ struct EncArgs {
     const int32_t* ctx_id;
     const uint64_t* x;
     int32_t stride;
+    int32_t x16;  // x is 16-byte aligned (then even strides allow 16-byte loads of a query)
     int64_t nq;
     uint64_t* words;
     uint8_t* qflags;
@@ -2150,24 +2151,40 @@ struct StageCtx {
 };
 
 // whole wavefront: stage context c (valid, fw <= 4) in the wavefront's LDS area
-__device__ __forceinline__ StageCtx stage_context(const EncArgs& e, int c, uint64_t* st) {
+// a context's scalars, all loads issued together (c valid)
+struct CtxScalars {
+    uint32_t flags;
+    int n, r0;
+    int64_t mo, bo, po;
+};
+__device__ __forceinline__ CtxScalars ctx_scalars(const EncArgs& e, int c) {
+    CtxScalars v;
+    v.flags = e.ctx_flags[c];
+    v.n = e.n_bits[c];
+    v.r0 = e.rank[c];
+    v.mo = e.map_off[c];
+    v.bo = e.basis_off[c];
+    v.po = e.piv_off[c];
+    return v;
+}
+
+__device__ __forceinline__ StageCtx stage_context(const EncArgs& e, const CtxScalars& v, uint64_t* st) {
     const int lane = threadIdx.x & 63;
     StageCtx g;
-    g.n = e.n_bits[c];
+    g.n = v.n;
     g.d = g.n + 1;
     g.fw = feat_words(g.n);
-    const int r0 = e.rank[c];
-    g.r = r0 < 0 ? 0 : (r0 > g.d ? g.d : r0);
+    g.r = v.r0 < 0 ? 0 : (v.r0 > g.d ? g.d : v.r0);
     g.rows = has_parity_rows(g.d, g.r);
     if (g.rows) {  // columns at words [0, 2d), the t fw words of parity-check rows at kEncStageRows
-        const uint64_t* M = e.maps + e.map_off[c];
-        const uint64_t* H = e.tables + e.basis_off[c];
+        const uint64_t* M = e.maps + v.mo;
+        const uint64_t* H = e.tables + v.bo;
         const int t = g.d - g.r;
         for (int k = lane; k < 2 * g.d; k += 64) st[k] = M[k];
         for (int k = lane; k < t * g.fw; k += 64) st[kEncStageRows + k] = H[k];
     } else {  // basis rows (r (fw + 2) words, r < d / 2 <= 128), then the pivots as words
-        const uint64_t* B = e.basis + e.basis_off[c];
-        const int32_t* P = e.pivots + e.piv_off[c];
+        const uint64_t* B = e.basis + v.bo;
+        const int32_t* P = e.pivots + v.po;
         const int nw = g.r * (g.fw + F2_Y_WORDS);
         for (int k = lane; k < nw; k += 64) st[k] = B[k];
         for (int k = lane; k < g.r; k += 64) st[nw + k] = static_cast<uint64_t>(P[k]);
@@ -2178,24 +2195,10 @@ __device__ __forceinline__ StageCtx stage_context(const EncArgs& e, int c, uint6
 
 template <int FW>
 __device__ __forceinline__ bool encode_staged(const EncArgs& e, const StageCtx& g, const uint64_t* st,
-                                              const uint64_t* xq, uint64_t& z0, uint64_t& z1) {
+                                              const uint64_t* xq, const uint64_t (&xv)[4], uint64_t& z0,
+                                              uint64_t& z1) {
     const int S = e.stride, n = g.n, d = g.d, fw = g.fw, cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
-    uint64_t xv[4] = {0, 0, 0, 0};
-    if (S == 2 || S == 4) {  // 16-byte loads (a query's words start 16-byte aligned)
-        const uint4* x4 = reinterpret_cast<const uint4*>(xq);
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            if (k >= S / 2) break;
-            const uint4 v = x4[k];
-            xv[2 * k] = (static_cast<uint64_t>(v.y) << 32) | v.x;
-            xv[2 * k + 1] = (static_cast<uint64_t>(v.w) << 32) | v.z;
-        }
-    } else {
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-            if (k < S) xv[k] = xq[k];
-    }
     bool outside = false;  // x bits at or above n
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
@@ -2295,27 +2298,49 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
     // one or two contexts; wider bins interleave their contexts' queries, and the
     // per-lane path serves them better
     const int nshared = s.bin_shift == 0 ? kSharedCtxPerWave : 0;
+    // the query's x words (up to 4) are loaded first: their latency overlaps the
+    // context's scalars and the staging
+    const uint64_t* xq = e.x + static_cast<int64_t>(live ? qc.x : 0) * e.stride;
+    uint64_t xv[4] = {0, 0, 0, 0};
+    if (nshared > 0 && live) {
+        const int S = e.stride;
+        if (e.x16 && (S == 2 || S == 4)) {  // 16-byte loads (a query's words start 16-byte aligned)
+            const uint4* x4 = reinterpret_cast<const uint4*>(xq);
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                if (k >= S / 2) break;
+                const uint4 v = x4[k];
+                xv[2 * k] = (static_cast<uint64_t>(v.y) << 32) | v.x;
+                xv[2 * k + 1] = (static_cast<uint64_t>(v.w) << 32) | v.z;
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                if (k < S) xv[k] = xq[k];
+        }
+    }
     for (int k = 0; k < nshared; ++k) {  // the wavefront's contexts, first lane's first
         const uint64_t todo = __ballot(!done);
         if (!todo) break;
         const int c0 = __builtin_amdgcn_readlane(qc.y, ffs64(todo));
-        if (c0 < 0 || c0 >= e.num_ctx || (e.ctx_flags[c0] & kBadCtx)) {
+        const bool valid = c0 >= 0 && c0 < e.num_ctx;
+        const CtxScalars v = ctx_scalars(e, valid ? c0 : 0);
+        if (!valid || (v.flags & kBadCtx)) {
             if (!done && qc.y == c0) {
                 fl.x = F2_Q_BAD_CTX;
                 done = true;
             }
             continue;
         }
-        if (feat_words(e.n_bits[c0]) > 4) break;  // wide: per-lane path
-        const StageCtx g = stage_context(e, c0, st);
+        if (feat_words(v.n) > 4) break;  // wide: per-lane path
+        const StageCtx g = stage_context(e, v, st);
         if (!done && qc.y == c0) {
-            fl.x = (e.ctx_flags[c0] & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0;
-            const uint64_t* xq = e.x + static_cast<int64_t>(qc.x) * e.stride;
+            fl.x = (v.flags & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0;
             bool in;
             switch (g.fw) {
-                case 1: in = encode_staged<1>(e, g, st, xq, out.x, out.y); break;
-                case 2: in = encode_staged<2>(e, g, st, xq, out.x, out.y); break;
-                default: in = encode_staged<4>(e, g, st, xq, out.x, out.y); break;
+                case 1: in = encode_staged<1>(e, g, st, xq, xv, out.x, out.y); break;
+                case 2: in = encode_staged<2>(e, g, st, xq, xv, out.x, out.y); break;
+                default: in = encode_staged<4>(e, g, st, xq, xv, out.x, out.y); break;
             }
             if (!in) {
                 fl.x |= F2_Q_OUT_OF_SPAN;
@@ -2741,6 +2766,7 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     e.ctx_id = ctx_id;
     e.x = x;
     e.stride = x_stride_words;
+    e.x16 = (reinterpret_cast<uintptr_t>(x) & 15u) == 0;
     e.nq = num_queries;
     e.words = words_out;
     e.qflags = qflags_out;

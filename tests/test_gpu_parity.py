@@ -408,6 +408,12 @@ def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
         torch.cuda.synchronize()
         parity.compare_encode(w2, q2, rw[a:b], rq[a:b])
     assert (rq & oracle.Q_BAD_CTX).sum() >= 3000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 1000
+    # x at an 8-byte (not 16-byte) aligned address: the grouped path reads words one at a time
+    xd = parity.to_dev(np.concatenate([np.zeros(1, np.uint64), x]))[1:]
+    assert xd.data_ptr() % 16 == 8
+    w3, q3 = f2.encode(model, parity.to_dev(ctx), xd, stride)
+    torch.cuda.synchronize()
+    parity.compare_encode(w3, q3, rw, rq)
 
 
 def _late_pivot_batch(seed, widths, rows_choices):
