@@ -2025,6 +2025,8 @@ struct SortArgs {
     int2* perm;       // [nq] sorted position -> (query, context id)
     int32_t* pos;     // [nq] query -> sorted position
     Word2* res;       // [2 nq] sorted position -> word, flags
+    int32_t regroup;  // 1: each chunk of kRegroupChunk positions regrouped by context (k_enc_regroup)
+    uint16_t* roff;   // [nq] regrouped position -> its position before, within the chunk (for res)
 };
 
 __device__ __forceinline__ int query_bin(const EncArgs& e, const SortArgs& s, int c) {
@@ -2127,6 +2129,90 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_scatter(EncArgs e, SortArg
     for (; q < q1; q += kSortThreads) {
         const int c = e.ctx_id[q];
         place(q, c, atomicAdd(&sBin[query_bin(e, s, c)], 1));
+    }
+}
+
+// A bin of 2^bin_shift contexts keeps its queries in batch order, so its contexts
+// interleave.  With many queries per context the sorted positions are regrouped
+// chunk by chunk (kRegroupChunk positions, in LDS): key = the bin's offset from
+// the chunk's first bin (clamped) and the context's low bits, so within a chunk
+// spanning few bins every context's entries end contiguous.  Entries only move
+// inside their chunk; roff keeps each one's former offset for the result slot.
+constexpr int kRegroupThreads = 1024;
+constexpr int kRegroupPer = 4;
+constexpr int kRegroupChunk = kRegroupThreads * kRegroupPer;  // 4096 positions, 12-bit keys
+
+__global__ __launch_bounds__(kRegroupThreads) void k_enc_regroup(EncArgs e, SortArgs s) {
+    __shared__ int sCount[kRegroupChunk];
+    __shared__ int sWave[kRegroupThreads / 64];
+    __shared__ int2 sEnt[kRegroupChunk];
+    __shared__ uint16_t sOff[kRegroupChunk];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kRegroupChunk;
+    const int n = e.nq - c0 < kRegroupChunk ? static_cast<int>(e.nq - c0) : kRegroupChunk;
+    const int b0 = query_bin(e, s, s.perm[c0].y);
+    const int lb = s.bin_shift < 12 ? s.bin_shift : 12;  // keys stay below kRegroupChunk
+    const int span = (kRegroupChunk >> lb) - 1;
+    int2 ent[kRegroupPer];
+    int key[kRegroupPer], rank[kRegroupPer];
+#pragma unroll
+    for (int u = 0; u < kRegroupPer; ++u) {
+        const int k = tid + u * kRegroupThreads;
+        ent[u] = k < n ? s.perm[c0 + k] : make_int2(0, 0);
+        sCount[k] = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kRegroupPer; ++u) {
+        const int k = tid + u * kRegroupThreads;
+        key[u] = 0;
+        rank[u] = 0;
+        if (k < n) {  // positions past the batch take no slot
+            const int db = query_bin(e, s, ent[u].y) - b0;  // >= 0: the chunk is in bin order
+            key[u] = ((db < span ? db : span) << lb) | (ent[u].y & ((1 << lb) - 1));
+            rank[u] = atomicAdd(&sCount[key[u]], 1);
+        }
+    }
+    __syncthreads();
+    // exclusive scan of the 4096 key counts: four consecutive keys per thread
+    int cnt[kRegroupPer], sum = 0;
+#pragma unroll
+    for (int u = 0; u < kRegroupPer; ++u) {
+        cnt[u] = sCount[kRegroupPer * tid + u];
+        sum += cnt[u];
+    }
+    int x = sum;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(x, o);
+        if (lane >= o) x += t;
+    }
+    if (lane == 63) sWave[wave] = x;
+    __syncthreads();
+    int base = x - sum;
+    for (int w = 0; w < wave; ++w) base += sWave[w];
+#pragma unroll
+    for (int u = 0; u < kRegroupPer; ++u) {
+        sCount[kRegroupPer * tid + u] = base;
+        base += cnt[u];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kRegroupPer; ++u) {
+        const int k = tid + u * kRegroupThreads;
+        if (k < n) {
+            const int dst = sCount[key[u]] + rank[u];
+            sEnt[dst] = ent[u];
+            sOff[dst] = static_cast<uint16_t>(k);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kRegroupPer; ++u) {
+        const int k = tid + u * kRegroupThreads;
+        if (k < n) {
+            s.perm[c0 + k] = sEnt[k];
+            if (!s.direct) s.roff[c0 + k] = sOff[k];
+        }
     }
 }
 
@@ -2294,10 +2380,10 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
     out.x = out.y = 0;
     fl.x = fl.y = 0;
     bool done = !live;
-    // with one context per bin the grouped order is exact and a wavefront holds
-    // one or two contexts; wider bins interleave their contexts' queries, and the
-    // per-lane path serves them better
-    const int nshared = s.bin_shift == 0 ? kSharedCtxPerWave : 0;
+    // with one context per bin, or after the regroup, a wavefront holds one or two
+    // contexts; otherwise a bin's contexts interleave, and the per-lane path
+    // serves them better
+    const int nshared = (s.bin_shift == 0 || s.regroup) ? kSharedCtxPerWave : 0;
     // the query's x words (up to 4) are loaded first: their latency overlaps the
     // context's scalars and the staging
     const uint64_t* xq = e.x + static_cast<int64_t>(live ? qc.x : 0) * e.stride;
@@ -2356,8 +2442,10 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
         *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
         e.qflags[qc.x] = static_cast<uint8_t>(fl.x);
     } else {
-        s.res[2 * i] = out;
-        s.res[2 * i + 1] = fl;
+        // the result slot is the position the scatter gave (the regroup moved the entry within its chunk)
+        const int64_t slot = s.regroup ? (i / kRegroupChunk) * kRegroupChunk + s.roff[i] : i;
+        s.res[2 * slot] = out;
+        s.res[2 * slot + 1] = fl;
     }
 }
 
@@ -2549,7 +2637,7 @@ unsigned fit_grid(int num_ctx, int cap) { return static_cast<unsigned>(num_ctx <
 struct EncPlan {
     bool sorted;
     SortArgs s;
-    size_t off_hist, off_total, off_base, off_perm, off_pos, off_res, bytes;
+    size_t off_hist, off_total, off_base, off_perm, off_pos, off_res, off_roff, bytes;
 };
 
 EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
@@ -2580,12 +2668,17 @@ EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     p.off_perm = o;
     o = align256(o + sizeof(int2) * static_cast<size_t>(nq));
     p.s.direct = nq <= kDirectMaxQueries;
+    // regroup when bins hold several contexts and contexts average 16 queries or more
+    p.s.regroup = shift > 0 && nq >= 16 * C;
     p.off_pos = o;
     p.off_res = o;
+    p.off_roff = o;
     if (!p.s.direct) {
         o = align256(o + sizeof(int32_t) * static_cast<size_t>(nq));
         p.off_res = o;
         o = align256(o + 2 * sizeof(Word2) * static_cast<size_t>(nq));
+        p.off_roff = o;
+        if (p.s.regroup) o = align256(o + sizeof(uint16_t) * static_cast<size_t>(nq));
     }
     p.bytes = o > 256 ? o : 256;
     return p;
@@ -2784,10 +2877,14 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     p.s.perm = reinterpret_cast<int2*>(ws + p.off_perm);
     p.s.pos = reinterpret_cast<int32_t*>(ws + p.off_pos);
     p.s.res = reinterpret_cast<Word2*>(ws + p.off_res);
+    p.s.roff = reinterpret_cast<uint16_t*>(ws + p.off_roff);
     hipLaunchKernelGGL(k_enc_count, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
     hipLaunchKernelGGL(k_enc_colscan, dim3((p.s.nb + 255) / 256), dim3(256), 0, s, p.s);
     hipLaunchKernelGGL(k_enc_binscan, dim3(1), dim3(kSortThreads), 0, s, p.s);
     hipLaunchKernelGGL(k_enc_scatter, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
+    if (p.s.regroup)
+        hipLaunchKernelGGL(k_enc_regroup, dim3(static_cast<unsigned>((num_queries + kRegroupChunk - 1) / kRegroupChunk)),
+                           dim3(kRegroupThreads), 0, s, e, p.s);
     hipLaunchKernelGGL(k_encode_sorted, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     if (!p.s.direct)
         hipLaunchKernelGGL(k_enc_unsort, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);

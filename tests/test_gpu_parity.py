@@ -280,6 +280,7 @@ def _encode_and_compare(f2, wl, model, ref, nq, stride, frac, zipf, sample=None)
     (2, 4096, 1_000_000, 2, 0.02, 0.0),
     (3, 80000, 1_000_000, 4, 0.01, 1.1),
     (3, 6000, 400_000, 4, 0.01, 1.1),   # one context per sort bin: the staged wavefront path, stride 4
+    (3, 10000, 400_000, 4, 0.01, 1.1),  # two contexts per bin, 40 queries per context: regrouped chunks
 ])
 def test_encode_recipes(f2, recipe, num_ctx, nq, stride, frac, zipf):
     wl = synth.fit_workload(recipe, num_ctx=num_ctx)
