@@ -2026,7 +2026,9 @@ struct SortArgs {
     int32_t* pos;     // [nq] query -> sorted position
     Word2* res;       // [2 nq] sorted position -> word, flags
     int32_t regroup;  // 1: each chunk of kRegroupChunk positions regrouped by context (k_enc_regroup)
+    int32_t staged;   // 1: k_encode_sorted stages the wavefronts' contexts; 0: every position per lane
     uint16_t* roff;   // [nq] regrouped position -> its position before, within the chunk (for res)
+    uint64_t* rest;   // [ceil(nq / 64)] positions the staged pass left to the per-lane pass (bit per lane)
 };
 
 __device__ __forceinline__ int query_bin(const EncArgs& e, const SortArgs& s, int c) {
@@ -2221,11 +2223,17 @@ __global__ __launch_bounds__(kRegroupThreads) void k_enc_regroup(EncArgs e, Sort
 // basis rows and pivots) are staged in LDS by the whole wavefront with coalesced
 // loads, and each lane masks the broadcast columns with its own phi bits: one
 // sign-extended bit per column, where the per-lane path gathers a column per
-// set bit with divergent addresses.  Staging capacity: contexts of up to 4
-// feature words (d <= 256); wider ones take the per-lane path.
-constexpr int kEncStageCols = 256;                // map columns (16 B each), words [0, 512)
-constexpr int kEncStageRows = 2 * kEncStageCols;  // first word of the parity-check rows (<= 128 x 4 words)
-constexpr int kEncStageWords = 4 * kEncStageCols; // words of one wavefront's stage (8 KB)
+// set bit with divergent addresses.  Staging capacity: contexts of up to 2
+// feature words (d <= 128); the positions of wider ones, and of wavefronts with
+// more than kSharedCtxPerWave contexts, are left to a per-lane pass (k_encode_rest),
+// which keeps this kernel's registers and LDS small (more wavefronts in flight
+// to cover its three dependent memory round trips: entry, context scalars, stage).
+constexpr int kEncStageFW = 2;
+constexpr int kEncStageCols = 64 * kEncStageFW;   // map columns (16 B each), words [0, 256)
+constexpr int kEncStageRows = 2 * kEncStageCols;  // first word of the parity-check rows (<= 64 x 2 words)
+constexpr int kEncStageWords = kEncStageRows + kEncStageCols / 2 * kEncStageFW;  // 3 KB per wavefront
+static_assert((kEncStageCols / 2 - 1) * (kEncStageFW + F2_Y_WORDS + 1) <= kEncStageWords,
+              "few-basis-row contexts (r < d / 2) fit the stage too");
 struct EncStage {
     uint64_t w[kEncThreads / 64][kEncStageWords];
 };
@@ -2236,7 +2244,7 @@ struct StageCtx {
     bool rows;  // parity-check rows (else: basis rows)
 };
 
-// whole wavefront: stage context c (valid, fw <= 4) in the wavefront's LDS area
+// whole wavefront: stage context c (valid, fw <= kEncStageFW) in the wavefront's LDS area
 // a context's scalars, all loads issued together (c valid)
 struct CtxScalars {
     uint32_t flags;
@@ -2268,7 +2276,7 @@ __device__ __forceinline__ StageCtx stage_context(const EncArgs& e, const CtxSca
         const int t = g.d - g.r;
         for (int k = lane; k < 2 * g.d; k += 64) st[k] = M[k];
         for (int k = lane; k < t * g.fw; k += 64) st[kEncStageRows + k] = H[k];
-    } else {  // basis rows (r (fw + 2) words, r < d / 2 <= 128), then the pivots as words
+    } else {  // basis rows (r (fw + 2) words, r < d / 2), then the pivots as words
         const uint64_t* B = e.basis + v.bo;
         const int32_t* P = e.pivots + v.po;
         const int nw = g.r * (g.fw + F2_Y_WORDS);
@@ -2380,15 +2388,11 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
     out.x = out.y = 0;
     fl.x = fl.y = 0;
     bool done = !live;
-    // with one context per bin, or after the regroup, a wavefront holds one or two
-    // contexts; otherwise a bin's contexts interleave, and the per-lane path
-    // serves them better
-    const int nshared = (s.bin_shift == 0 || s.regroup) ? kSharedCtxPerWave : 0;
     // the query's x words (up to 4) are loaded first: their latency overlaps the
     // context's scalars and the staging
     const uint64_t* xq = e.x + static_cast<int64_t>(live ? qc.x : 0) * e.stride;
     uint64_t xv[4] = {0, 0, 0, 0};
-    if (nshared > 0 && live) {
+    if (live) {
         const int S = e.stride;
         if (e.x16 && (S == 2 || S == 4)) {  // 16-byte loads (a query's words start 16-byte aligned)
             const uint4* x4 = reinterpret_cast<const uint4*>(xq);
@@ -2405,7 +2409,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
                 if (k < S) xv[k] = xq[k];
         }
     }
-    for (int k = 0; k < nshared; ++k) {  // the wavefront's contexts, first lane's first
+    for (int k = 0; k < kSharedCtxPerWave; ++k) {  // the wavefront's contexts, first lane's first
         const uint64_t todo = __ballot(!done);
         if (!todo) break;
         const int c0 = __builtin_amdgcn_readlane(qc.y, ffs64(todo));
@@ -2418,16 +2422,13 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
             }
             continue;
         }
-        if (feat_words(v.n) > 4) break;  // wide: per-lane path
+        if (feat_words(v.n) > kEncStageFW) break;  // wider: per-lane pass
         const StageCtx g = stage_context(e, v, st);
         if (!done && qc.y == c0) {
             fl.x = (v.flags & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0;
             bool in;
-            switch (g.fw) {
-                case 1: in = encode_staged<1>(e, g, st, xq, xv, out.x, out.y); break;
-                case 2: in = encode_staged<2>(e, g, st, xq, xv, out.x, out.y); break;
-                default: in = encode_staged<4>(e, g, st, xq, xv, out.x, out.y); break;
-            }
+            if (g.fw == 1) in = encode_staged<1>(e, g, st, xq, xv, out.x, out.y);
+            else in = encode_staged<2>(e, g, st, xq, xv, out.x, out.y);
             if (!in) {
                 fl.x |= F2_Q_OUT_OF_SPAN;
                 out.x = out.y = 0;
@@ -2436,13 +2437,34 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
         }
         wave_sync();  // the stage is rewritten for the next context
     }
-    if (!done) fl.x = encode_one(e, qc.y, qc.x, out.x, out.y);  // lanes of further contexts
-    if (!live) return;
+    const uint64_t left = __ballot(!done);  // lanes of further or wider contexts: per-lane pass
+    if ((threadIdx.x & 63) == 0 && i < e.nq) s.rest[i >> 6] = left;
+    if (!done || !live) return;
     if (s.direct) {
         *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
         e.qflags[qc.x] = static_cast<uint8_t>(fl.x);
     } else {
         // the result slot is the position the scatter gave (the regroup moved the entry within its chunk)
+        const int64_t slot = s.regroup ? (i / kRegroupChunk) * kRegroupChunk + s.roff[i] : i;
+        s.res[2 * slot] = out;
+        s.res[2 * slot + 1] = fl;
+    }
+}
+
+// the per-lane pass over the grouped order: every position (s.staged = 0), or the
+// positions the staged pass left (their bits in s.rest)
+__global__ __launch_bounds__(kEncThreads) void k_encode_rest(EncArgs e, SortArgs s) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
+    if (i >= e.nq) return;
+    if (s.staged && !((s.rest[i >> 6] >> (threadIdx.x & 63)) & 1ull)) return;
+    const int2 qc = s.perm[i];
+    Word2 out, fl;
+    fl.x = encode_one(e, qc.y, qc.x, out.x, out.y);
+    fl.y = 0;
+    if (s.direct) {
+        *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
+        e.qflags[qc.x] = static_cast<uint8_t>(fl.x);
+    } else {
         const int64_t slot = s.regroup ? (i / kRegroupChunk) * kRegroupChunk + s.roff[i] : i;
         s.res[2 * slot] = out;
         s.res[2 * slot + 1] = fl;
@@ -2637,7 +2659,7 @@ unsigned fit_grid(int num_ctx, int cap) { return static_cast<unsigned>(num_ctx <
 struct EncPlan {
     bool sorted;
     SortArgs s;
-    size_t off_hist, off_total, off_base, off_perm, off_pos, off_res, off_roff, bytes;
+    size_t off_hist, off_total, off_base, off_perm, off_rest, off_pos, off_res, off_roff, bytes;
 };
 
 EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
@@ -2670,6 +2692,11 @@ EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     p.s.direct = nq <= kDirectMaxQueries;
     // regroup when bins hold several contexts and contexts average 16 queries or more
     p.s.regroup = shift > 0 && nq >= 16 * C;
+    // with one context per bin, or after the regroup, a wavefront holds one or two
+    // contexts and the staged pass applies; otherwise every position goes per lane
+    p.s.staged = shift == 0 || p.s.regroup;
+    p.off_rest = o;
+    o = align256(o + sizeof(uint64_t) * static_cast<size_t>((nq + 63) / 64));
     p.off_pos = o;
     p.off_res = o;
     p.off_roff = o;
@@ -2878,6 +2905,7 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     p.s.pos = reinterpret_cast<int32_t*>(ws + p.off_pos);
     p.s.res = reinterpret_cast<Word2*>(ws + p.off_res);
     p.s.roff = reinterpret_cast<uint16_t*>(ws + p.off_roff);
+    p.s.rest = reinterpret_cast<uint64_t*>(ws + p.off_rest);
     hipLaunchKernelGGL(k_enc_count, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
     hipLaunchKernelGGL(k_enc_colscan, dim3((p.s.nb + 255) / 256), dim3(256), 0, s, p.s);
     hipLaunchKernelGGL(k_enc_binscan, dim3(1), dim3(kSortThreads), 0, s, p.s);
@@ -2885,7 +2913,9 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     if (p.s.regroup)
         hipLaunchKernelGGL(k_enc_regroup, dim3(static_cast<unsigned>((num_queries + kRegroupChunk - 1) / kRegroupChunk)),
                            dim3(kRegroupThreads), 0, s, e, p.s);
-    hipLaunchKernelGGL(k_encode_sorted, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
+    if (p.s.staged)
+        hipLaunchKernelGGL(k_encode_sorted, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
+    hipLaunchKernelGGL(k_encode_rest, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     if (!p.s.direct)
         hipLaunchKernelGGL(k_enc_unsort, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
