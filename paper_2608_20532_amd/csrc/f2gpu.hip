@@ -677,8 +677,19 @@ __device__ __forceinline__ uint64_t sel_word(const uint64_t (&f)[FW], int wi) {
     return v;
 }
 
+// Four-Russians tables for contexts of up to 4 feature words (d <= 256): their
+// records use rec[0, 256), and the tables take the rest of rec plus tabx (the
+// two are adjacent): table g holds the 16 XOR combinations of the retained rows
+// of positions 4g .. 4g+3 (fw + 2 words each; absent pivots contribute zero)
+constexpr int kPivTabExtra = 1480;  // keeps three workgroups per compute unit within the LDS
+constexpr int kPivTabWords = (kPivCap / 2) * kPivRec + kPivTabExtra;
+constexpr int kPivTabMinRank = 32;   // smaller bases reduce as fast record by record
+constexpr int kPivTabMinRows = 512;  // tables are built only with two rounds of rows or more to go
+
 struct PivShared {
     uint64_t rec[kPivCap][kPivRec];
+    uint64_t tabx[kPivTabExtra];  // continues rec (tables)
+    int ntab;                     // valid tables (positions [0, 4 ntab)), 0: none
     uint64_t pm[kPivMaxFW];   // pivot columns of the retained rows
     uint64_t npm[kPivMaxFW];  // pivot columns of the rows the current round added
     int flag[kPivWaves];
@@ -686,14 +697,69 @@ struct PivShared {
     long long first, round_first;
 };
 
-// reduce this wavefront's block rows against the retained basis (one pass: the basis is fully reduced)
+// all threads: the tables of the first positions (as many as fit) from the records
+template <int FW, int NW>
+__device__ __forceinline__ void piv_build_tables(PivShared& S, int d) {
+    constexpr int W = FW + F2_Y_WORDS;
+    constexpr int cap = kPivTabWords / (16 * W);
+    const int nt = (d + 3) / 4 < cap ? (d + 3) / 4 : cap;
+    uint64_t* tab = &S.rec[kPivCap / 2][0];
+    for (int t = threadIdx.x; t < nt * W; t += 64 * NW) {  // one (table, word) per step
+        const int g = t / W, w = t - g * W;
+        uint64_t* e = tab + g * 16 * W + w;  // entry k of table g at e[k W]
+        e[0] = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int p = 4 * g + b;
+            const bool piv = p < d && ((S.pm[p >> 6] >> (p & 63)) & 1ull);
+            const uint64_t r = piv ? S.rec[p][w] : 0ull;
+            for (int k = 0; k < (1 << b); ++k) e[((1 << b) + k) * W] = e[k * W] ^ r;
+        }
+    }
+    if (threadIdx.x == 0) S.ntab = nt;
+}
+
+// reduce this wavefront's block rows against the retained basis (one pass: the
+// basis is fully reduced).  Positions [0, 4 ntab) by table lookups: the row's own
+// 4 bits at positions 4g .. 4g+3, masked to the pivots, select entry of table g.
 template <int FW>
-__device__ __forceinline__ void piv_reduce(PivShared& S, int fw, uint64_t (&f)[FW], uint64_t& y0, uint64_t& y1) {
+__device__ __forceinline__ void piv_reduce(PivShared& S, int fw, int ntab, uint64_t (&f)[FW], uint64_t& y0,
+                                           uint64_t& y1) {
+    constexpr int W = FW + F2_Y_WORDS;
     uint64_t f0[FW];
 #pragma unroll
     for (int w = 0; w < FW; ++w) f0[w] = f[w];
-    for (int pw = 0; pw < fw; ++pw) {
+    if constexpr (FW <= 4) {
+        const uint64_t* tab = &S.rec[kPivCap / 2][0];
+#pragma unroll
+        for (int w = 0; w < FW; ++w) {
+            if (16 * w >= ntab) break;
+            const uint64_t pmw = S.pm[w];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const uint32_t half = h ? static_cast<uint32_t>(f0[w] >> 32) : static_cast<uint32_t>(f0[w]);
+                const uint32_t pmh = h ? static_cast<uint32_t>(pmw >> 32) : static_cast<uint32_t>(pmw);
+#pragma unroll 1
+                for (int k = 0; k < 8; k += 2) {  // two tables per step, one three-way XOR per word
+                    const int g = 16 * w + 8 * h + k;
+                    if (g >= ntab) break;
+                    const uint32_t i0 = __builtin_amdgcn_ubfe(half, 4 * k, 4) & ((pmh >> (4 * k)) & 0xFu);
+                    uint32_t i1 = __builtin_amdgcn_ubfe(half, 4 * k + 4, 4) & ((pmh >> (4 * k + 4)) & 0xFu);
+                    if (g + 1 >= ntab) i1 = 0;  // past the last table: entry 0 of table g (zero)
+                    const uint64_t* e0 = tab + (16 * g + static_cast<int>(i0)) * W;
+                    const uint64_t* e1 = tab + (16 * (g + 1 < ntab ? g + 1 : g) + static_cast<int>(i1)) * W;
+#pragma unroll
+                    for (int u = 0; u < FW; ++u) f[u] = xor3(f[u], e0[u], e1[u]);
+                    y0 = xor3(y0, e0[FW], e1[FW]);
+                    y1 = xor3(y1, e0[FW + 1], e1[FW + 1]);
+                }
+            }
+        }
+    }
+    const int done = FW <= 4 ? 4 * ntab : 0;  // positions below are reduced
+    for (int pw = done >> 6; pw < fw; ++pw) {
         uint64_t pm = S.pm[pw];
+        if (pw == (done >> 6) && (done & 63)) pm &= ~0ull << (done & 63);
         if (!pm) continue;
         const uint64_t ow = sel_word<FW>(f0, pw);  // unreduced word pw of this lane's row
         while (pm) {
@@ -846,6 +912,7 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
     if (tid == 0) {
         S.contra = 0;
         S.nnew = 0;
+        S.ntab = 0;
         S.first = -1;
     }
     __syncthreads();
@@ -892,7 +959,13 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
             if (w == fw - 1) f[w] &= tmask;
         y0 = valid ? raw[FW] : 0ull;
         y1 = valid ? raw[FW + 1] : 0ull;
-        if (rank > 0) piv_reduce<FW>(S, fw, f, y0, y1);
+        if constexpr (FW <= 4) {  // a large basis that will serve two rounds or more: tables
+            if (S.ntab == 0 && rank >= kPivTabMinRank && m - b0 >= kPivTabMinRows) {
+                piv_build_tables<FW, NW>(S, d);
+                __syncthreads();
+            }
+        }
+        if (rank > 0) piv_reduce<FW>(S, fw, S.ntab, f, y0, y1);
         uint64_t any = f[0];
 #pragma unroll
         for (int w = 1; w < FW; ++w) any |= f[w];
@@ -923,6 +996,7 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
             piv_backsub<FW, NW>(S, d, fw);
             __syncthreads();
             if (tid < fw) S.pm[tid] |= S.npm[tid];
+            if (tid == 0) S.ntab = 0;  // the tables no longer match the basis
             __syncthreads();
         }
         if (tid == 0 && S.first < 0 && S.round_first != 0x7fffffffffffffffll) S.first = S.round_first;
@@ -1718,7 +1792,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
 // The list (largest first) is taken greedily: workgroup g starts at position g,
 // then each takes the next free position from a counter as it finishes one (the
 // fetch is issued when a context starts, so its latency hides behind the work).
-__global__ __launch_bounds__(kPivThreads) void k_fit_piv(FitArgs a) {
+__global__ __launch_bounds__(kPivThreads, 3) void k_fit_piv(FitArgs a) {
     __shared__ PivShared S;
     __shared__ int sNext;
     const int lo = a.plan[kClsPiv], cnt = a.plan[kClsPivLong + 1] - lo;
