@@ -660,9 +660,11 @@ __global__ __launch_bounds__(64 * kRegWaves) void k_fit_reg(FitArgs a) {
 // kernel runs kPivWaves) the next NW blocks of 64 rows are reduced
 // in parallel, one per wavefront; the first block (in stream order) that still
 // holds a nonzero feature residual runs the insertion loop in its own
-// wavefront, the blocks before it are only classified, the blocks after it are
-// redone against the grown basis.  Once the basis stops growing every round
-// completes NW blocks.
+// wavefront (in registers), the blocks before it are only classified, the
+// blocks after it are redone against the grown basis; then every wavefront
+// clears the new pivots from the retained records.  Once the basis stops
+// growing every round completes NW blocks, and a large basis reduces through
+// Four-Russians tables.
 // ---------------------------------------------------------------------------
 constexpr int kPivRec = kPivMaxFW + F2_Y_WORDS;  // record words
 constexpr int kPivCap = 64 * kPivMaxFW;          // d <= 512
