@@ -417,7 +417,7 @@ def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
     parity.compare_encode(w3, q3, rw, rq)
 
 
-def _late_pivot_batch(seed, widths, rows_choices):
+def _late_pivot_batch(seed, widths, rows_choices, kmax=40):
     """Long contexts whose rows first span a small subspace and only later reveal new
     pivots (one generator added every few hundred rows), with contradictions late."""
     rng = np.random.default_rng(seed)
@@ -427,7 +427,7 @@ def _late_pivot_batch(seed, widths, rows_choices):
         fw = (n + 64) // 64
         d = n + 1
         m = int(rng.choice(rows_choices))
-        k = int(rng.integers(1, min(d, 40) + 1))
+        k = int(rng.integers(1, min(d, kmax) + 1))
         pool = rng.integers(0, 2 ** 63, size=(k, fw), dtype=np.uint64) ^ (rng.integers(0, 2, size=(k, fw), dtype=np.uint64) << np.uint64(63))
         vb = d - 64 * (fw - 1)
         if vb < 64:
@@ -450,3 +450,11 @@ def test_fit_long_contexts_late_pivots(f2):
     rng = np.random.default_rng(31)
     widths = [int(w) for w in rng.integers(0, 512, size=40)] + [0, 63, 64, 127, 191, 192, 255, 256, 319, 447, 511]
     _fit_and_compare(f2, _late_pivot_batch(31, widths, [200, 257, 300, 700, 1500, 2600]))
+
+
+def test_fit_long_high_rank_contexts(f2):
+    """Long contexts of 2-4 feature words whose rank grows past 100 over many rounds: the
+    LDS basis reduces through Four-Russians tables (rebuilt after each growth), for widths
+    whose positions outrun the tables too (d = 256)."""
+    widths = [100, 130, 150, 191, 200, 230, 250, 255, 254, 180, 120, 240]
+    _fit_and_compare(f2, _late_pivot_batch(57, widths, [1100, 1800, 3000], kmax=256))
