@@ -694,7 +694,7 @@ struct PivShared {
     int ntab;                     // valid tables (positions [0, 4 ntab)), 0: none
     uint64_t pm[kPivMaxFW];   // pivot columns of the retained rows
     uint64_t npm[kPivMaxFW];  // pivot columns of the rows the current round added
-    int flag[kPivWaves];
+    int flag[8];  // per wavefront (up to 8)
     int contra, nnew;
     long long first, round_first;
 };
@@ -1816,6 +1816,55 @@ __global__ __launch_bounds__(kPivThreads, 3) void k_fit_piv(FitArgs a) {
     }
 }
 
+// Small batches (up to kSmallBatch contexts): one launch, one workgroup of 8
+// wavefronts per context, the context's class choosing the path (one wavefront
+// for the register basis, all eight for the LDS basis and the wide path, which
+// runs here as a group of one workgroup).  No plan: its two launches would cost
+// more than the fit of a batch this size, and one workgroup per context needs no
+// load balance.  Invalid contexts are flagged here.
+constexpr int kSmallBatch = 64;
+union SmallShared {
+    struct {
+        uint64_t rec[64 * kRegMaxFW * kRecWords];
+        int16_t pos[64 * kRegMaxFW];
+    } reg;
+    PivShared piv;
+    LargeShared large;
+};
+
+__global__ __launch_bounds__(kLargeThreads) void k_fit_small(FitArgs a) {
+    __shared__ SmallShared U;
+    const CtxDesc ds = readlane_desc(load_desc(a, blockIdx.x), 0);
+    if (ds.c < 0) return;
+    if (ds.bad) {
+        if (threadIdx.x == 0) write_bad_context(a, ds);
+        return;
+    }
+    const int fw = feat_words(ds.n);
+    switch (fit_class(ds)) {
+        case kClsReg:
+            if (threadIdx.x < 64) {
+                if (fw == 1) fit_ctx_reg<1>(a, ds, U.reg.rec, U.reg.pos);
+                else if (fw == 2) fit_ctx_reg<2>(a, ds, U.reg.rec, U.reg.pos);
+                else fit_ctx_reg<3>(a, ds, U.reg.rec, U.reg.pos);
+            }
+            break;
+        case kClsLarge: {
+            int epoch = 0;
+            fit_ctx_large(a, ds, U.large, 1, 0, a.plan + kBarHead, epoch);
+            break;
+        }
+        default:
+            switch (fw) {
+                case 1: fit_ctx_piv<1, kLargeWaves>(a, ds, U.piv); break;
+                case 2: fit_ctx_piv<2, kLargeWaves>(a, ds, U.piv); break;
+                case 3: case 4: fit_ctx_piv<4, kLargeWaves>(a, ds, U.piv); break;
+                default: fit_ctx_piv<8, kLargeWaves>(a, ds, U.piv); break;
+            }
+            break;
+    }
+}
+
 // Wide contexts (class 3): with few of them (as many as a quarter of the
 // workgroups or fewer) each is fitted by a group of 4 workgroups, by 2 with up to
 // half, else by one.  Under a cooperative launch every workgroup is resident,
@@ -2852,6 +2901,11 @@ int wide_resident_workgroups() {
 constexpr int kPivGrid = 768;  // LDS-basis workgroups: three per compute unit (LDS-bound)
 void launch_fit(FitArgs a, hipStream_t s) {
     const int32_t C = a.num_ctx;
+    if (C <= kSmallBatch) {
+        a.coop = 0;
+        hipLaunchKernelGGL(k_fit_small, dim3(static_cast<unsigned>(C)), dim3(kLargeThreads), 0, s, a);
+        return;
+    }
     const int plan_blocks = static_cast<int>((static_cast<int64_t>(C) + kPlanThreads - 1) / kPlanThreads);
     hipLaunchKernelGGL(k_plan_count, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a);
     hipLaunchKernelGGL(k_plan_scatter, dim3(plan_blocks), dim3(kPlanThreads), 0, s, a, plan_blocks);
