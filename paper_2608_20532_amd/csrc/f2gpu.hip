@@ -1816,12 +1816,12 @@ __global__ __launch_bounds__(kPivThreads, 3) void k_fit_piv(FitArgs a) {
     }
 }
 
-// Small batches (up to kSmallBatch contexts): one launch, one workgroup of 8
-// wavefronts per context, the context's class choosing the path (one wavefront
-// for the register basis, all eight for the LDS basis and the wide path, which
-// runs here as a group of one workgroup).  No plan: its two launches would cost
-// more than the fit of a batch this size, and one workgroup per context needs no
-// load balance.  Invalid contexts are flagged here.
+// Small batches (up to kSmallBatch contexts, declared widths below 512): one
+// launch, one workgroup of 8 wavefronts per context, the context's class choosing
+// the path (one wavefront for the register basis, all eight for the LDS basis).
+// No plan: its two launches would cost more than the fit of a batch this size,
+// and one workgroup per context needs no load balance.  Invalid contexts, and any
+// wider than the declared bound, are flagged here.
 constexpr int kSmallBatch = 64;
 union SmallShared {
     struct {
@@ -1829,7 +1829,6 @@ union SmallShared {
         int16_t pos[64 * kRegMaxFW];
     } reg;
     PivShared piv;
-    LargeShared large;
 };
 
 __global__ __launch_bounds__(kLargeThreads) void k_fit_small(FitArgs a) {
@@ -1849,11 +1848,8 @@ __global__ __launch_bounds__(kLargeThreads) void k_fit_small(FitArgs a) {
                 else fit_ctx_reg<3>(a, ds, U.reg.rec, U.reg.pos);
             }
             break;
-        case kClsLarge: {
-            int epoch = 0;
-            fit_ctx_large(a, ds, U.large, 1, 0, a.plan + kBarHead, epoch);
+        case kClsLarge:  // not launched for a batch that may hold one (the bound is below 512)
             break;
-        }
         default:
             switch (fw) {
                 case 1: fit_ctx_piv<1, kLargeWaves>(a, ds, U.piv); break;
@@ -2901,7 +2897,7 @@ int wide_resident_workgroups() {
 constexpr int kPivGrid = 768;  // LDS-basis workgroups: three per compute unit (LDS-bound)
 void launch_fit(FitArgs a, hipStream_t s) {
     const int32_t C = a.num_ctx;
-    if (C <= kSmallBatch) {
+    if (C <= kSmallBatch && a.max_n >= 0 && a.max_n < 512) {
         a.coop = 0;
         hipLaunchKernelGGL(k_fit_small, dim3(static_cast<unsigned>(C)), dim3(kLargeThreads), 0, s, a);
         return;
