@@ -16,7 +16,9 @@
  * ---------------------------------------
  *  - Every pointer argument is DEVICE memory allocated and owned by the
  *    caller unless its name ends in _host.  The library allocates nothing and
- *    keeps no state between calls; concurrent calls need distinct workspaces.
+ *    keeps no state between calls (beyond a per-device cache of how many
+ *    workgroups of the wide-context fit can be resident at once, queried on
+ *    first use); concurrent calls need distinct workspaces.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
  *    device work is enqueued on it; outputs are valid once it has synchronised.
  *  - A negative return value means nothing was enqueued (argument errors that
