@@ -2607,19 +2607,29 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_unsort(EncArgs e, SortArgs 
 // ---------------------------------------------------------------------------
 constexpr int kStreamThreads = 256;
 
+// each workgroup writes the kVecRows rows from blockIdx * kVecRows on; the row of
+// an output word is its index in the workgroup's span times magic = ceil(2^32 / rw)
+// (exact: the span is under 2^15 words and rw <= 66)
+constexpr int kVecRows = 256;
+
 __global__ __launch_bounds__(kStreamThreads) void k_vectorize(const uint64_t* values, const uint64_t* y,
                                                               int64_t num_rows, int k, uint64_t keep0,
-                                                              uint64_t keep1, uint64_t* rows) {
+                                                              uint64_t keep1, uint64_t* rows, uint32_t magic) {
     const int rw = k + 3;
-    const int64_t o = static_cast<int64_t>(blockIdx.x) * kStreamThreads + threadIdx.x;
-    if (o >= num_rows * rw) return;
-    const int64_t r = o / rw;
-    const int j = static_cast<int>(o - r * rw);
-    uint64_t v;
-    if (j < k) v = values[r * k + j];
-    else if (j == k) v = 1;  // the constant feature
-    else v = y ? (y[2 * r + (j - k - 1)] & (j == k + 1 ? keep0 : keep1)) : 0ull;
-    rows[o] = v;
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kVecRows;
+    const int nr = num_rows - r0 < kVecRows ? static_cast<int>(num_rows - r0) : kVecRows;
+    const uint64_t* vals = values + r0 * k;
+    const uint64_t* yr = y ? y + 2 * r0 : nullptr;
+    uint64_t* out = rows + r0 * rw;
+    for (int w = threadIdx.x; w < nr * rw; w += kStreamThreads) {
+        const int r = static_cast<int>(__umulhi(static_cast<uint32_t>(w), magic));
+        const int j = w - r * rw;
+        uint64_t v;
+        if (j < k) v = vals[r * k + j];
+        else if (j == k) v = 1;  // the constant feature
+        else v = yr ? (yr[2 * r + (j - k - 1)] & (j == k + 1 ? keep0 : keep1)) : 0ull;
+        out[w] = v;
+    }
 }
 
 __global__ __launch_bounds__(kStreamThreads) void k_merge(const uint64_t* words, const uint64_t* field, int shift,
@@ -3053,11 +3063,13 @@ int f2_vectorize_rows(const uint64_t* values, const uint64_t* y, int64_t num_row
     if (num_rows < 0 || k < 0 || k > 63 || !keep_host) return F2_EINVAL;
     if (num_rows == 0) return F2_OK;
     if ((k > 0 && !values) || !rows_out) return F2_EINVAL;
-    const int64_t total = num_rows * (k + 3);
-    const int64_t blocks = (total + kStreamThreads - 1) / kStreamThreads;
+    const int64_t blocks = (num_rows + kVecRows - 1) / kVecRows;
     if (num_rows > (int64_t{1} << 56) || blocks > 0x7fffffff) return F2_EINVAL;
+    const uint32_t rw = static_cast<uint32_t>(k + 3);
+    const uint32_t magic = static_cast<uint32_t>(((uint64_t{1} << 32) + rw - 1) / rw);  // ceil(2^32 / rw)
     hipLaunchKernelGGL(k_vectorize, dim3(static_cast<unsigned>(blocks)), dim3(kStreamThreads), 0,
-                       static_cast<hipStream_t>(stream), values, y, num_rows, k, keep_host[0], keep_host[1], rows_out);
+                       static_cast<hipStream_t>(stream), values, y, num_rows, k, keep_host[0], keep_host[1], rows_out,
+                       magic);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 
