@@ -2125,10 +2125,12 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs e) {
 // pass returns the results to query order (up to kDirectMaxQueries queries the
 // results are written straight to their queries instead: scattered writes of a
 // batch that size merge in the last-level cache, larger ones pay for the extra
-// pass with coalesced writes).  The sort uses per-block LDS
-// histograms and scans (no device-wide atomics):
-//   count (per block)  ->  column scan (per bin, over blocks)  ->  bin scan
-//   ->  scatter (query -> sorted position)  ->  sorted encode  ->  unsort
+// pass with coalesced writes; the sorted passes then store the 16-byte word and
+// an out-of-span bit per result, and the unsort takes the other flags from the
+// context).  The sort uses per-block LDS histograms and scans (no device-wide
+// counters):
+//   count (per block)  ->  column scan (per bin, over blocks)  ->  scatter (bin
+//   scan per block, query -> sorted position)  ->  sorted encode  ->  unsort
 // ---------------------------------------------------------------------------
 constexpr int kSortThreads = 1024;
 constexpr int kSortMaxBins = 8192;
@@ -2142,14 +2144,16 @@ struct SortArgs {
     int64_t qc;       // queries per count / scatter block
     int32_t* hist;    // [blocks][nb], then exclusive offsets within each bin
     int32_t* total;   // [nb]
-    int32_t* base;    // [nb] first sorted position of each bin
     int2* perm;       // [nq] sorted position -> (query, context id)
     int32_t* pos;     // [nq] query -> sorted position
-    Word2* res;       // [2 nq] sorted position -> word, flags
+    Word2* res;       // [nq] result slot -> word
+    uint64_t* oos;    // [ceil(nq / 64)] result slot -> out of span (bit per slot; cleared by the count)
     int32_t regroup;  // 1: each chunk of kRegroupChunk positions regrouped by context (k_enc_regroup)
     int32_t staged;   // 1: k_encode_sorted stages the wavefronts' contexts; 0: every position per lane
     uint16_t* roff;   // [nq] regrouped position -> its position before, within the chunk (for res)
-    uint64_t* rest;   // [ceil(nq / 64)] positions the staged pass left to the per-lane pass (bit per lane)
+    uint64_t* rest;   // [ceil(nq / 64)] positions the staged pass left to the second pass (bit per lane)
+    int32_t* rest_list;   // [ceil(nq / 64)] the 64-position groups with such positions, in no order
+    int32_t* rest_count;  // [1] entries of rest_list (cleared by the count)
 };
 
 __device__ __forceinline__ int query_bin(const EncArgs& e, const SortArgs& s, int c) {
@@ -2172,6 +2176,9 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_count(EncArgs e, SortArgs 
         for (int u = 0; u < 4; ++u) atomicAdd(&sBin[query_bin(e, s, c[u])], 1);
     }
     for (; q < q1; q += kSortThreads) atomicAdd(&sBin[query_bin(e, s, e.ctx_id[q])], 1);
+    if (!s.direct)  // the out-of-span bits of the block's slots (a word shared with the next block gets two zero stores)
+        for (int64_t w = (q0 >> 6) + tid; w < ((q1 + 63) >> 6); w += kSortThreads) s.oos[w] = 0;
+    if (blockIdx.x == 0 && tid == 0) *s.rest_count = 0;
     __syncthreads();
     int32_t* h = s.hist + static_cast<int64_t>(blockIdx.x) * s.nb;
     for (int b = tid; b < s.nb; b += kSortThreads) h[b] = sBin[b];
@@ -2202,15 +2209,21 @@ __global__ __launch_bounds__(256) void k_enc_colscan(SortArgs s) {
     s.total[b] = run;
 }
 
-// one workgroup: exclusive scan of the bin totals
-__global__ __launch_bounds__(kSortThreads) void k_enc_binscan(SortArgs s) {
-    __shared__ int sWave[kSortThreads / 64];
+// exclusive scan of the bin totals by one workgroup of kSortThreads threads,
+// added into sBin, which holds the block's own offsets within each bin (h, copied
+// here while the totals are loading)
+constexpr int kBinsPerThread = (kSortMaxBins + 1 + kSortThreads - 1) / kSortThreads;
+__device__ __forceinline__ void bin_offsets(const SortArgs& s, const int32_t* h, int* sBin, int* sWave) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int per = (s.nb + kSortThreads - 1) / kSortThreads;
     const int b0 = tid * per;
+    int tv[kBinsPerThread];
+#pragma unroll
+    for (int k = 0; k < kBinsPerThread; ++k) tv[k] = (k < per && b0 + k < s.nb) ? s.total[b0 + k] : 0;
+    for (int b = tid; b < s.nb; b += kSortThreads) sBin[b] = h[b];
     int sum = 0;
-    for (int k = 0; k < per; ++k)
-        if (b0 + k < s.nb) sum += s.total[b0 + k];
+#pragma unroll
+    for (int k = 0; k < kBinsPerThread; ++k) sum += tv[k];
     int x = sum;
     for (int o = 1; o < 64; o <<= 1) {
         const int t = __shfl_up(x, o);
@@ -2220,18 +2233,21 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_binscan(SortArgs s) {
     __syncthreads();
     int run = x - sum;
     for (int w = 0; w < (tid >> 6); ++w) run += sWave[w];
-    for (int k = 0; k < per; ++k)
-        if (b0 + k < s.nb) {
-            s.base[b0 + k] = run;
-            run += s.total[b0 + k];
+#pragma unroll
+    for (int k = 0; k < kBinsPerThread; ++k)
+        if (k < per && b0 + k < s.nb) {
+            sBin[b0 + k] += run;
+            run += tv[k];
         }
 }
 
 __global__ __launch_bounds__(kSortThreads) void k_enc_scatter(EncArgs e, SortArgs s) {
     __shared__ int sBin[kSortMaxBins + 1];
+    __shared__ int sWave[kSortThreads / 64];
     const int tid = threadIdx.x;
-    const int32_t* h = s.hist + static_cast<int64_t>(blockIdx.x) * s.nb;
-    for (int b = tid; b < s.nb; b += kSortThreads) sBin[b] = s.base[b] + h[b];
+    // every block scans the bin totals itself (a few thousand words) instead of a
+    // one-workgroup scan kernel between the column scan and the scatter
+    bin_offsets(s, s.hist + static_cast<int64_t>(blockIdx.x) * s.nb, sBin, sWave);
     __syncthreads();
     const int64_t q0 = static_cast<int64_t>(blockIdx.x) * s.qc;
     const int64_t q1 = q0 + s.qc < e.nq ? q0 + s.qc : e.nq;
@@ -2346,17 +2362,31 @@ __global__ __launch_bounds__(kRegroupThreads) void k_enc_regroup(EncArgs e, Sort
 // sign-extended bit per column, where the per-lane path gathers a column per
 // set bit with divergent addresses.  Staging capacity: contexts of up to 2
 // feature words (d <= 128); the positions of wider ones, and of wavefronts with
-// more than kSharedCtxPerWave contexts, are left to a per-lane pass (k_encode_rest),
+// more than kSharedCtxPerWave contexts, are left to a second pass (k_encode_rest),
 // which keeps this kernel's registers and LDS small (more wavefronts in flight
 // to cover its three dependent memory round trips: entry, context scalars, stage).
-constexpr int kEncStageFW = 2;
-constexpr int kEncStageCols = 64 * kEncStageFW;   // map columns (16 B each), words [0, 256)
-constexpr int kEncStageRows = 2 * kEncStageCols;  // first word of the parity-check rows (<= 64 x 2 words)
-constexpr int kEncStageWords = kEncStageRows + kEncStageCols / 2 * kEncStageFW;  // 3 KB per wavefront
-static_assert((kEncStageCols / 2 - 1) * (kEncStageFW + F2_Y_WORDS + 1) <= kEncStageWords,
-              "few-basis-row contexts (r < d / 2) fit the stage too");
+// The second pass stages, in a stage of up to 4 feature words, each context that
+// holds at least kRestStageLanes of a wavefront's remaining lanes, and gathers per
+// lane for the others.
+//
+// A stage of SFW feature words: 64 SFW map columns of 16 bytes at words
+// [0, 128 SFW), the parity-check rows (fewer than d / 2 + 1 of up to SFW words)
+// from word 128 SFW; or, with few basis rows (r < d / 2), the basis rows and then
+// the pivots as words.
+template <int SFW>
+struct StageGeom {
+    static constexpr int cols = 64 * SFW;
+    static constexpr int rows = 2 * cols;                  // first word of the parity-check rows
+    static constexpr int words = rows + cols / 2 * SFW;    // SFW = 2: 3 KB, SFW = 4: 8 KB
+    static_assert((cols / 2 - 1) * (SFW + F2_Y_WORDS + 1) <= words, "few-basis-row contexts fit the stage too");
+};
+constexpr int kEncStageFW = 2;  // the staged pass
+constexpr int kEncWideFW = 4;   // the second pass
 struct EncStage {
-    uint64_t w[kEncThreads / 64][kEncStageWords];
+    uint64_t w[kEncThreads / 64][StageGeom<kEncStageFW>::words];
+};
+struct EncStageWide {
+    uint64_t w[kEncThreads / 64][StageGeom<kEncWideFW>::words];
 };
 
 // the staged context's geometry (uniform)
@@ -2365,7 +2395,6 @@ struct StageCtx {
     bool rows;  // parity-check rows (else: basis rows)
 };
 
-// whole wavefront: stage context c (valid, fw <= kEncStageFW) in the wavefront's LDS area
 // a context's scalars, all loads issued together (c valid)
 struct CtxScalars {
     uint32_t flags;
@@ -2380,9 +2409,14 @@ __device__ __forceinline__ CtxScalars ctx_scalars(const EncArgs& e, int c) {
     v.mo = e.map_off[c];
     v.bo = e.basis_off[c];
     v.po = e.piv_off[c];
+    // all six values taken here: the six loads go out together (else each is
+    // sunk to its first use, behind the branches on the ones before)
+    __asm__ volatile("" : : "s"(v.flags), "s"(v.n), "s"(v.r0), "s"(v.mo), "s"(v.bo), "s"(v.po));
     return v;
 }
 
+// whole wavefront: stage the context of v (valid, fw <= SFW) in the wavefront's LDS area
+template <int SFW>
 __device__ __forceinline__ StageCtx stage_context(const EncArgs& e, const CtxScalars& v, uint64_t* st) {
     const int lane = threadIdx.x & 63;
     StageCtx g;
@@ -2391,24 +2425,47 @@ __device__ __forceinline__ StageCtx stage_context(const EncArgs& e, const CtxSca
     g.fw = feat_words(g.n);
     g.r = v.r0 < 0 ? 0 : (v.r0 > g.d ? g.d : v.r0);
     g.rows = has_parity_rows(g.d, g.r);
-    if (g.rows) {  // columns at words [0, 2d), the t fw words of parity-check rows at kEncStageRows
+    // every load of the stage is issued before the first LDS store (one round trip)
+    using G = StageGeom<SFW>;
+    if (g.rows) {  // columns at words [0, 2d), the t fw words of parity-check rows from G::rows
+        constexpr int NM = 2 * G::cols / 64, NH = (G::words - G::rows) / 64;  // words per lane (d <= cols, t <= d / 2)
         const uint64_t* M = e.maps + v.mo;
         const uint64_t* H = e.tables + v.bo;
-        const int t = g.d - g.r;
-        for (int k = lane; k < 2 * g.d; k += 64) st[k] = M[k];
-        for (int k = lane; k < t * g.fw; k += 64) st[kEncStageRows + k] = H[k];
+        const int nm = 2 * g.d, nh = (g.d - g.r) * g.fw;
+        uint64_t a[NM], b[NH];
+#pragma unroll
+        for (int u = 0; u < NM; ++u) a[u] = lane + 64 * u < nm ? M[lane + 64 * u] : 0ull;
+#pragma unroll
+        for (int u = 0; u < NH; ++u) b[u] = lane + 64 * u < nh ? H[lane + 64 * u] : 0ull;
+#pragma unroll
+        for (int u = 0; u < NM; ++u)
+            if (lane + 64 * u < nm) st[lane + 64 * u] = a[u];
+#pragma unroll
+        for (int u = 0; u < NH; ++u)
+            if (lane + 64 * u < nh) st[G::rows + lane + 64 * u] = b[u];
     } else {  // basis rows (r (fw + 2) words, r < d / 2), then the pivots as words
+        constexpr int NB = (G::cols / 2 * (SFW + F2_Y_WORDS) + 63) / 64, NP = (G::cols / 2 + 63) / 64;
         const uint64_t* B = e.basis + v.bo;
         const int32_t* P = e.pivots + v.po;
         const int nw = g.r * (g.fw + F2_Y_WORDS);
-        for (int k = lane; k < nw; k += 64) st[k] = B[k];
-        for (int k = lane; k < g.r; k += 64) st[nw + k] = static_cast<uint64_t>(P[k]);
+        uint64_t a[NB];
+        int32_t b[NP];
+#pragma unroll
+        for (int u = 0; u < NB; ++u) a[u] = lane + 64 * u < nw ? B[lane + 64 * u] : 0ull;
+#pragma unroll
+        for (int u = 0; u < NP; ++u) b[u] = lane + 64 * u < g.r ? P[lane + 64 * u] : 0;
+#pragma unroll
+        for (int u = 0; u < NB; ++u)
+            if (lane + 64 * u < nw) st[lane + 64 * u] = a[u];
+#pragma unroll
+        for (int u = 0; u < NP; ++u)
+            if (lane + 64 * u < g.r) st[nw + lane + 64 * u] = static_cast<uint64_t>(b[u]);
     }
     wave_sync();
     return g;
 }
 
-template <int FW>
+template <int FW, int SFW>
 __device__ __forceinline__ bool encode_staged(const EncArgs& e, const StageCtx& g, const uint64_t* st,
                                               const uint64_t* xq, const uint64_t (&xv)[4], uint64_t& z0,
                                               uint64_t& z1) {
@@ -2421,42 +2478,41 @@ __device__ __forceinline__ bool encode_staged(const EncArgs& e, const StageCtx& 
         if (w > cw) outside |= xv[w] != 0;
         else if (w == cw) outside |= (xv[w] >> (n & 63)) != 0;
     }
-    for (int w = 4; w < S; ++w) outside |= xq[w] != 0;  // staged contexts have fw <= 2: all of these are outside
+    for (int w = 4; w < S; ++w) outside |= xq[w] != 0;  // staged contexts have fw <= 4: all of these are outside
     uint64_t ph[FW];
 #pragma unroll
     for (int w = 0; w < FW; ++w) ph[w] = (w < fw ? xv[w] : 0ull) | (w == cw ? cbit : 0ull);
     if (g.rows) {
         // T(phi): every staged column, masked by its bit of phi (the columns past
-        // n hold stale words, and their mask is zero)
+        // n hold stale words, and their mask is zero).  A loop over 32-column
+        // steps, unrolled within a step: fully unrolled, the code of every width
+        // runs to several KB per wavefront and instruction fetch bounds the pass.
         const uint4* col = reinterpret_cast<const uint4*>(st);
         uint32_t a0 = 0, a1 = 0, a2 = 0, a3 = 0;
+#pragma unroll 1
+        for (int j0 = 0; j0 < d; j0 += 32) {
+            uint64_t pw = ph[0];
 #pragma unroll
-        for (int w = 0; w < FW; ++w) {
-            if (w >= fw) break;
+            for (int k = 1; k < FW; ++k) pw = (j0 >> 6) == k ? ph[k] : pw;
+            const uint32_t half = static_cast<uint32_t>(pw >> (j0 & 32));
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const uint32_t half = h ? static_cast<uint32_t>(ph[w] >> 32) : static_cast<uint32_t>(ph[w]);
-                const int j0 = 64 * w + 32 * h;
-                if (j0 >= d) break;
+            for (int u0 = 0; u0 < 32; u0 += 8) {
+                if (j0 + u0 >= d) break;
 #pragma unroll
-                for (int u0 = 0; u0 < 32; u0 += 8) {
-                    if (j0 + u0 >= d) break;
-#pragma unroll
-                    for (int u = u0; u < u0 + 8; ++u) {
-                        const uint4 v = col[j0 + u];
-                        const uint32_t mk = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(half), u, 1));
-                        a0 = __builtin_amdgcn_bitop3_b32(a0, mk, v.x, 0x78);
-                        a1 = __builtin_amdgcn_bitop3_b32(a1, mk, v.y, 0x78);
-                        a2 = __builtin_amdgcn_bitop3_b32(a2, mk, v.z, 0x78);
-                        a3 = __builtin_amdgcn_bitop3_b32(a3, mk, v.w, 0x78);
-                    }
+                for (int u = u0; u < u0 + 8; ++u) {
+                    const uint4 v = col[j0 + u];
+                    const uint32_t mk = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(half), u, 1));
+                    a0 = __builtin_amdgcn_bitop3_b32(a0, mk, v.x, 0x78);
+                    a1 = __builtin_amdgcn_bitop3_b32(a1, mk, v.y, 0x78);
+                    a2 = __builtin_amdgcn_bitop3_b32(a2, mk, v.z, 0x78);
+                    a3 = __builtin_amdgcn_bitop3_b32(a3, mk, v.w, 0x78);
                 }
             }
         }
         z0 = (static_cast<uint64_t>(a1) << 32) | a0;
         z1 = (static_cast<uint64_t>(a3) << 32) | a2;
         // support: even overlap with every parity-check row
-        const uint64_t* H = st + kEncStageRows;
+        const uint64_t* H = st + StageGeom<SFW>::rows;
         const int t = d - g.r;
         uint32_t odd = 0;
         for (int f = 0; f < t; ++f) {
@@ -2499,6 +2555,26 @@ __device__ __forceinline__ bool encode_staged(const EncArgs& e, const StageCtx& 
 
 constexpr int kSharedCtxPerWave = 4;  // contexts of a wavefront taken through the stage
 
+// a query's first x words (up to 4), 16 bytes at a time where the stride and
+// the alignment allow
+__device__ __forceinline__ void load_x4(const EncArgs& e, const uint64_t* xq, uint64_t (&xv)[4]) {
+    const int S = e.stride;
+    if (e.x16 && (S == 2 || S == 4)) {  // a query's words start 16-byte aligned
+        const uint4* x4 = reinterpret_cast<const uint4*>(xq);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            if (k >= S / 2) break;
+            const uint4 v = x4[k];
+            xv[2 * k] = (static_cast<uint64_t>(v.y) << 32) | v.x;
+            xv[2 * k + 1] = (static_cast<uint64_t>(v.w) << 32) | v.z;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (k < S) xv[k] = xq[k];
+    }
+}
+
 __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortArgs s) {
     __shared__ EncStage sStage;
     const int64_t i = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
@@ -2513,23 +2589,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
     // context's scalars and the staging
     const uint64_t* xq = e.x + static_cast<int64_t>(live ? qc.x : 0) * e.stride;
     uint64_t xv[4] = {0, 0, 0, 0};
-    if (live) {
-        const int S = e.stride;
-        if (e.x16 && (S == 2 || S == 4)) {  // 16-byte loads (a query's words start 16-byte aligned)
-            const uint4* x4 = reinterpret_cast<const uint4*>(xq);
-#pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                if (k >= S / 2) break;
-                const uint4 v = x4[k];
-                xv[2 * k] = (static_cast<uint64_t>(v.y) << 32) | v.x;
-                xv[2 * k + 1] = (static_cast<uint64_t>(v.w) << 32) | v.z;
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                if (k < S) xv[k] = xq[k];
-        }
-    }
+    if (live) load_x4(e, xq, xv);
     for (int k = 0; k < kSharedCtxPerWave; ++k) {  // the wavefront's contexts, first lane's first
         const uint64_t todo = __ballot(!done);
         if (!todo) break;
@@ -2544,12 +2604,10 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
             continue;
         }
         if (feat_words(v.n) > kEncStageFW) break;  // wider: per-lane pass
-        const StageCtx g = stage_context(e, v, st);
+        const StageCtx g = stage_context<kEncStageFW>(e, v, st);
         if (!done && qc.y == c0) {
             fl.x = (v.flags & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0;
-            bool in;
-            if (g.fw == 1) in = encode_staged<1>(e, g, st, xq, xv, out.x, out.y);
-            else in = encode_staged<2>(e, g, st, xq, xv, out.x, out.y);
+            const bool in = encode_staged<kEncStageFW, kEncStageFW>(e, g, st, xq, xv, out.x, out.y);
             if (!in) {
                 fl.x |= F2_Q_OUT_OF_SPAN;
                 out.x = out.y = 0;
@@ -2558,8 +2616,11 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
         }
         wave_sync();  // the stage is rewritten for the next context
     }
-    const uint64_t left = __ballot(!done);  // lanes of further or wider contexts: per-lane pass
-    if ((threadIdx.x & 63) == 0 && i < e.nq) s.rest[i >> 6] = left;
+    const uint64_t left = __ballot(!done);  // lanes of further or wider contexts: second pass
+    if ((threadIdx.x & 63) == 0 && i < e.nq) {
+        s.rest[i >> 6] = left;
+        if (left) s.rest_list[atomicAdd(s.rest_count, 1)] = static_cast<int32_t>(i >> 6);  // a few percent of the groups
+    }
     if (!done || !live) return;
     if (s.direct) {
         *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
@@ -2567,28 +2628,103 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
     } else {
         // the result slot is the position the scatter gave (the regroup moved the entry within its chunk)
         const int64_t slot = s.regroup ? (i / kRegroupChunk) * kRegroupChunk + s.roff[i] : i;
-        s.res[2 * slot] = out;
-        s.res[2 * slot + 1] = fl;
+        s.res[slot] = out;
+        if (fl.x & F2_Q_OUT_OF_SPAN) atomicOr(&s.oos[slot >> 6], 1ull << (slot & 63));
     }
 }
 
-// the per-lane pass over the grouped order: every position (s.staged = 0), or the
-// positions the staged pass left (their bits in s.rest)
-__global__ __launch_bounds__(kEncThreads) void k_encode_rest(EncArgs e, SortArgs s) {
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
-    if (i >= e.nq) return;
-    if (s.staged && !((s.rest[i >> 6] >> (threadIdx.x & 63)) & 1ull)) return;
-    const int2 qc = s.perm[i];
-    Word2 out, fl;
-    fl.x = encode_one(e, qc.y, qc.x, out.x, out.y);
-    fl.y = 0;
+// the second pass over the grouped order: the positions the staged pass left
+// (their groups in s.rest_list, their lanes in s.rest).  A context holding at
+// least kRestStageLanes of the wavefront's remaining lanes (and up to kEncWideFW
+// feature words) is staged; the other lanes gather per lane.  A fixed grid whose
+// wavefronts take the listed groups in turn: a grid over every position would
+// launch (and allocate the stage for) a workgroup per 256 positions, almost all
+// of them idle (1.2 against 0.42 ms on 100M queries).
+constexpr int kRestStageLanes = 16;
+constexpr int kRestCtxPerWave = 4;  // contexts of a wavefront considered for the stage
+constexpr int kRestGrid = 1024;     // workgroups of the listed-group pass
+
+// one wavefront: the lanes of bits among positions i0 .. i0 + 63
+__device__ __forceinline__ void rest_group(const EncArgs& e, const SortArgs& s, uint64_t* st, int64_t i0,
+                                           uint64_t bits) {
+    const int lane = threadIdx.x & 63;
+    const int64_t i = i0 + lane;
+    const bool live = i < e.nq && ((bits >> lane) & 1ull);
+    if (!__ballot(live)) return;
+    const int2 qc = live ? s.perm[i] : make_int2(0, 0);
+    const int64_t slot = (live && !s.direct && s.regroup) ? (i / kRegroupChunk) * kRegroupChunk + s.roff[i] : i;
+    const uint64_t* xq = e.x + static_cast<int64_t>(live ? qc.x : 0) * e.stride;
+    uint64_t xv[4] = {0, 0, 0, 0};
+    if (live) load_x4(e, xq, xv);
+    Word2 out;
+    out.x = out.y = 0;
+    uint8_t fl = 0;
+    bool done = !live, lane_path = false;
+    for (int k = 0; k < kRestCtxPerWave; ++k) {
+        const uint64_t todo = __ballot(!done && !lane_path);
+        if (!todo) break;
+        const int c0 = __builtin_amdgcn_readlane(qc.y, ffs64(todo));
+        const bool mine = !done && !lane_path && qc.y == c0;
+        bool stage = c0 >= 0 && c0 < e.num_ctx && __popcll(__ballot(mine)) >= kRestStageLanes;
+        CtxScalars v;
+        if (stage) {
+            v = ctx_scalars(e, c0);
+            stage = !(v.flags & kBadCtx) && feat_words(v.n) <= kEncWideFW;
+        }
+        if (!stage) {  // few lanes, or a bad or wide context: per lane
+            if (mine) lane_path = true;
+            continue;
+        }
+        const StageCtx g = stage_context<kEncWideFW>(e, v, st);
+        if (mine) {
+            fl = (v.flags & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0;
+            const bool in = encode_staged<kEncWideFW, kEncWideFW>(e, g, st, xq, xv, out.x, out.y);
+            if (!in) {
+                fl |= F2_Q_OUT_OF_SPAN;
+                out.x = out.y = 0;
+            }
+            done = true;
+        }
+        wave_sync();  // the stage is rewritten for the next context
+    }
+    if (!done) fl = encode_one(e, qc.y, qc.x, out.x, out.y);
+    if (!live) return;
     if (s.direct) {
         *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
-        e.qflags[qc.x] = static_cast<uint8_t>(fl.x);
+        e.qflags[qc.x] = fl;
     } else {
-        const int64_t slot = s.regroup ? (i / kRegroupChunk) * kRegroupChunk + s.roff[i] : i;
-        s.res[2 * slot] = out;
-        s.res[2 * slot + 1] = fl;
+        s.res[slot] = out;
+        if (fl & F2_Q_OUT_OF_SPAN) atomicOr(&s.oos[slot >> 6], 1ull << (slot & 63));
+    }
+}
+
+__global__ __launch_bounds__(kEncThreads) void k_encode_rest(EncArgs e, SortArgs s) {
+    __shared__ EncStageWide sStage;
+    const int wave = threadIdx.x >> 6;
+    uint64_t* st = sStage.w[wave];
+    const int cnt = *s.rest_count;
+    const int waves = static_cast<int>(gridDim.x) * (kEncThreads / 64);
+    for (int k = static_cast<int>(blockIdx.x) * (kEncThreads / 64) + wave; k < cnt; k += waves) {
+        const int g = __builtin_amdgcn_readfirstlane(s.rest_list[k]);
+        rest_group(e, s, st, static_cast<int64_t>(g) * 64, s.rest[g]);
+    }
+}
+
+// grouped order without the staged pass (bins of several contexts, not
+// regrouped): every position per lane, the lanes of a wavefront gathering from
+// the few maps of its bins
+__global__ __launch_bounds__(kEncThreads) void k_encode_lanes(EncArgs e, SortArgs s) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
+    if (i >= e.nq) return;
+    const int2 qc = s.perm[i];
+    Word2 out;
+    const uint8_t fl = encode_one(e, qc.y, qc.x, out.x, out.y);
+    if (s.direct) {
+        *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
+        e.qflags[qc.x] = fl;
+    } else {
+        s.res[i] = out;
+        if (fl & F2_Q_OUT_OF_SPAN) atomicOr(&s.oos[i >> 6], 1ull << (i & 63));
     }
 }
 
@@ -2596,8 +2732,19 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_unsort(EncArgs e, SortArgs 
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
     if (q >= e.nq) return;
     const int64_t i = s.pos[q];
-    *reinterpret_cast<Word2*>(e.words + 2 * q) = s.res[2 * i];
-    e.qflags[q] = static_cast<uint8_t>(s.res[2 * i + 1].x);
+    const int c = e.ctx_id[q];
+    const Word2 w = s.res[i];
+    const uint64_t o = s.oos[i >> 6];
+    // the flags again from the context (bad, contradictory) and the slot's out-of-span bit
+    uint8_t fl = F2_Q_BAD_CTX;
+    if (c >= 0 && c < e.num_ctx) {
+        const uint32_t cf = e.ctx_flags[c];
+        if (!(cf & kBadCtx))
+            fl = ((cf & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0) |
+                 (((o >> (i & 63)) & 1ull) ? F2_Q_OUT_OF_SPAN : 0);
+    }
+    *reinterpret_cast<Word2*>(e.words + 2 * q) = w;
+    e.qflags[q] = fl;
 }
 
 // ---------------------------------------------------------------------------
@@ -2790,7 +2937,7 @@ unsigned fit_grid(int num_ctx, int cap) { return static_cast<unsigned>(num_ctx <
 struct EncPlan {
     bool sorted;
     SortArgs s;
-    size_t off_hist, off_total, off_base, off_perm, off_rest, off_pos, off_res, off_roff, bytes;
+    size_t off_hist, off_total, off_perm, off_rest, off_rest_list, off_rest_count, off_pos, off_res, off_oos, off_roff, bytes;
 };
 
 EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
@@ -2817,8 +2964,6 @@ EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     o = align256(o + sizeof(int32_t) * static_cast<size_t>(p.s.blocks) * p.s.nb);
     p.off_total = o;
     o = align256(o + sizeof(int32_t) * p.s.nb);
-    p.off_base = o;
-    o = align256(o + sizeof(int32_t) * p.s.nb);
     p.off_perm = o;
     o = align256(o + sizeof(int2) * static_cast<size_t>(nq));
     p.s.direct = nq <= kDirectMaxQueries;
@@ -2829,13 +2974,20 @@ EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     p.s.staged = shift == 0 || p.s.regroup;
     p.off_rest = o;
     o = align256(o + sizeof(uint64_t) * static_cast<size_t>((nq + 63) / 64));
+    p.off_rest_list = o;
+    o = align256(o + sizeof(int32_t) * static_cast<size_t>((nq + 63) / 64));
+    p.off_rest_count = o;
+    o = align256(o + sizeof(int32_t));
     p.off_pos = o;
     p.off_res = o;
     p.off_roff = o;
+    p.off_oos = o;
     if (!p.s.direct) {
         o = align256(o + sizeof(int32_t) * static_cast<size_t>(nq));
         p.off_res = o;
-        o = align256(o + 2 * sizeof(Word2) * static_cast<size_t>(nq));
+        o = align256(o + sizeof(Word2) * static_cast<size_t>(nq));
+        p.off_oos = o;
+        o = align256(o + sizeof(uint64_t) * static_cast<size_t>((nq + 63) / 64));
         p.off_roff = o;
         if (p.s.regroup) o = align256(o + sizeof(uint16_t) * static_cast<size_t>(nq));
     }
@@ -3037,22 +3189,27 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     char* ws = static_cast<char*>(workspace);
     p.s.hist = reinterpret_cast<int32_t*>(ws + p.off_hist);
     p.s.total = reinterpret_cast<int32_t*>(ws + p.off_total);
-    p.s.base = reinterpret_cast<int32_t*>(ws + p.off_base);
     p.s.perm = reinterpret_cast<int2*>(ws + p.off_perm);
     p.s.pos = reinterpret_cast<int32_t*>(ws + p.off_pos);
     p.s.res = reinterpret_cast<Word2*>(ws + p.off_res);
+    p.s.oos = reinterpret_cast<uint64_t*>(ws + p.off_oos);
     p.s.roff = reinterpret_cast<uint16_t*>(ws + p.off_roff);
     p.s.rest = reinterpret_cast<uint64_t*>(ws + p.off_rest);
+    p.s.rest_list = reinterpret_cast<int32_t*>(ws + p.off_rest_list);
+    p.s.rest_count = reinterpret_cast<int32_t*>(ws + p.off_rest_count);
     hipLaunchKernelGGL(k_enc_count, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
     hipLaunchKernelGGL(k_enc_colscan, dim3((p.s.nb + 255) / 256), dim3(256), 0, s, p.s);
-    hipLaunchKernelGGL(k_enc_binscan, dim3(1), dim3(kSortThreads), 0, s, p.s);
     hipLaunchKernelGGL(k_enc_scatter, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
     if (p.s.regroup)
         hipLaunchKernelGGL(k_enc_regroup, dim3(static_cast<unsigned>((num_queries + kRegroupChunk - 1) / kRegroupChunk)),
                            dim3(kRegroupThreads), 0, s, e, p.s);
-    if (p.s.staged)
+    if (p.s.staged) {
         hipLaunchKernelGGL(k_encode_sorted, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
-    hipLaunchKernelGGL(k_encode_rest, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
+        hipLaunchKernelGGL(k_encode_rest, dim3(static_cast<unsigned>(blocks < kRestGrid ? blocks : kRestGrid)),
+                           dim3(kEncThreads), 0, s, e, p.s);
+    } else {
+        hipLaunchKernelGGL(k_encode_lanes, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
+    }
     if (!p.s.direct)
         hipLaunchKernelGGL(k_enc_unsort, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;

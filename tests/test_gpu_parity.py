@@ -375,11 +375,9 @@ def test_encode_grouped_path_random_widths(f2):
     assert (rq == 0).sum() > 1000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 1000 and (rq & oracle.Q_BAD_CTX).any()
 
 
-def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
-    """One query batch through the context-grouped path (whole batch) and the per-query path
-    (slices below its size threshold), against the oracle, with malformed contexts in the
-    model and context ids out of range."""
-    import torch
+def _bad_context_model(f2):
+    """40 contexts of recipe 2's shape with two malformed ones (1: too wide; 3: a segment
+    that is not a whole number of rows), fitted on the GPU; returns (wl, oracle fit, model)."""
     wl = synth.fit_workload(2, num_ctx=40)
     n_bits = wl.n_bits.copy()
     row_off = wl.row_off.copy()
@@ -392,13 +390,28 @@ def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
     nb = f2.f2_fit_workspace_bytes(model.num_ctx)
     ws = f2.workspace(nb)
     assert f2.f2_fit_batch(parity.to_dev(wl.rows), wl.rows.size, parity.to_dev(row_off), model, ws, nb) == 0
-    nq, stride = 240_000, 2   # the whole batch is grouped (196,608 queries or more), its halves are not
+    return wl, ref, model
+
+
+def _bad_context_queries(wl, nq, stride, seed):
+    """Queries of recipe 2's stream with ids out of range and queries of the malformed contexts."""
     ctx, x, _ = synth.queries(wl, nq, stride, 0.05, 0.0)
-    rng = np.random.default_rng(41)
+    rng = np.random.default_rng(seed)
     idx = rng.choice(nq, size=3000, replace=False)
     ctx[idx[:1000]] = rng.choice(np.array([-1, 40, 12345, -7], np.int32), size=1000)
     ctx[idx[1000:2000]] = 1
     ctx[idx[2000:]] = 3
+    return ctx, x
+
+
+def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
+    """One query batch through the context-grouped path (whole batch) and the per-query path
+    (slices below its size threshold), against the oracle, with malformed contexts in the
+    model and context ids out of range."""
+    import torch
+    wl, ref, model = _bad_context_model(f2)
+    nq, stride = 240_000, 2   # the whole batch is grouped (196,608 queries or more), its halves are not
+    ctx, x = _bad_context_queries(wl, nq, stride, 41)
     rw, rq = oracle.encode_batch(ref, ctx, x, stride)
     words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x), stride)    # grouped path
     torch.cuda.synchronize()
@@ -415,6 +428,22 @@ def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
     w3, q3 = f2.encode(model, parity.to_dev(ctx), xd, stride)
     torch.cuda.synchronize()
     parity.compare_encode(w3, q3, rw, rq)
+
+
+def test_encode_results_through_the_unsort_with_bad_contexts(f2):
+    """A batch above 4,194,304 queries: the grouped passes keep 16-byte words and an
+    out-of-span bit per result, and the pass back to query order rebuilds the flags from
+    the context; every query is checked, bad contexts and ids out of range included."""
+    import torch
+    wl, ref, model = _bad_context_model(f2)
+    nq, stride = 4_300_000, 2
+    ctx, x = _bad_context_queries(wl, nq, stride, 43)
+    rw, rq = oracle.encode_batch(ref, ctx, x, stride)
+    words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x), stride)
+    torch.cuda.synchronize()
+    parity.compare_encode(words, qf, rw, rq)
+    assert (rq & oracle.Q_BAD_CTX).sum() >= 3000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 100_000
+    assert (rq & oracle.Q_CTX_CONTRADICTORY).any() and (rq == 0).sum() > 1_000_000
 
 
 def _late_pivot_batch(seed, widths, rows_choices, kmax=40):
