@@ -2184,29 +2184,41 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_count(EncArgs e, SortArgs 
     for (int b = tid; b < s.nb; b += kSortThreads) h[b] = sBin[b];
 }
 
-// one thread per bin: exclusive prefix over the blocks, in place; the bin's total
-__global__ __launch_bounds__(256) void k_enc_colscan(SortArgs s) {
-    const int b = blockIdx.x * 256 + threadIdx.x;
+// exclusive prefix of each bin over the blocks, in place, and the bin's total.
+// A workgroup takes 64 bins (a lane each) and splits the blocks among its 16
+// wavefronts, so every lane has all of its loads in flight at once.
+constexpr int kColWaves = 16;
+constexpr int kMaxSortBlocks = 256;
+constexpr int kColPerWave = kMaxSortBlocks / kColWaves;  // blocks per wavefront (at most)
+__global__ __launch_bounds__(64 * kColWaves) void k_enc_colscan(SortArgs s) {
+    __shared__ int sPart[kColWaves][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int b = blockIdx.x * 64 + lane;
+    const int per = (s.blocks + kColWaves - 1) / kColWaves;  // <= kColPerWave
+    const int gb = wave * per;
+    int v[kColPerWave];
+#pragma unroll
+    for (int k = 0; k < kColPerWave; ++k)
+        v[k] = (b < s.nb && k < per && gb + k < s.blocks) ? s.hist[static_cast<int64_t>(gb + k) * s.nb + b] : 0;
+    int sum = 0;
+#pragma unroll
+    for (int k = 0; k < kColPerWave; ++k) sum += v[k];
+    sPart[wave][lane] = sum;
+    __syncthreads();
+    int run = 0, total = 0;
+    for (int w = 0; w < kColWaves; ++w) {
+        const int t = sPart[w][lane];
+        run += w < wave ? t : 0;
+        total += t;
+    }
     if (b >= s.nb) return;
-    int run = 0;
-    int g = 0;
-    for (; g + 8 <= s.blocks; g += 8) {  // eight loads in flight
-        int v[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) v[k] = s.hist[static_cast<int64_t>(g + k) * s.nb + b];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            s.hist[static_cast<int64_t>(g + k) * s.nb + b] = run;
+    for (int k = 0; k < kColPerWave; ++k)
+        if (k < per && gb + k < s.blocks) {
+            s.hist[static_cast<int64_t>(gb + k) * s.nb + b] = run;
             run += v[k];
         }
-    }
-    for (; g < s.blocks; ++g) {
-        int32_t* h = s.hist + static_cast<int64_t>(g) * s.nb + b;
-        const int v = *h;
-        *h = run;
-        run += v;
-    }
-    s.total[b] = run;
+    if (wave == 0) s.total[b] = total;
 }
 
 // exclusive scan of the bin totals by one workgroup of kSortThreads threads,
@@ -2955,7 +2967,7 @@ EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     // up to 256 count / scatter blocks of at least 8k queries: enough blocks for the
     // scatter, few histogram rows to scan (1M queries: 83 us with 8k, 86 with 16k, 88 with 4k)
     int64_t blocks = (nq + 8191) / 8192;
-    if (blocks > 256) blocks = 256;
+    if (blocks > kMaxSortBlocks) blocks = kMaxSortBlocks;
     const int64_t qc = (nq + blocks - 1) / blocks;
     p.s.qc = qc;
     p.s.blocks = static_cast<int>((nq + qc - 1) / qc);
@@ -3198,7 +3210,7 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     p.s.rest_list = reinterpret_cast<int32_t*>(ws + p.off_rest_list);
     p.s.rest_count = reinterpret_cast<int32_t*>(ws + p.off_rest_count);
     hipLaunchKernelGGL(k_enc_count, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
-    hipLaunchKernelGGL(k_enc_colscan, dim3((p.s.nb + 255) / 256), dim3(256), 0, s, p.s);
+    hipLaunchKernelGGL(k_enc_colscan, dim3((p.s.nb + 63) / 64), dim3(64 * kColWaves), 0, s, p.s);
     hipLaunchKernelGGL(k_enc_scatter, dim3(p.s.blocks), dim3(kSortThreads), 0, s, e, p.s);
     if (p.s.regroup)
         hipLaunchKernelGGL(k_enc_regroup, dim3(static_cast<unsigned>((num_queries + kRegroupChunk - 1) / kRegroupChunk)),
