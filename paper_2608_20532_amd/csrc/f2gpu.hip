@@ -804,39 +804,42 @@ __device__ void piv_insert(PivShared& S, int n, int64_t b0, bool valid, uint64_t
     const int lane = threadIdx.x & 63;
     const int cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
+    uint64_t xm[FW];  // the x columns of each feature word (the constant column cleared)
+#pragma unroll
+    for (int w = 0; w < FW; ++w) xm[w] = (w == cw) ? ~cbit : ~0ull;
+    if (lane < FW) S.npm[lane] = 0;
     uint64_t pending = __ballot(valid);
     uint64_t ins = 0;  // lanes holding new basis rows
-    uint64_t npm[FW];  // their pivot columns
-#pragma unroll
-    for (int w = 0; w < FW; ++w) npm[w] = 0;
-    int mypiv = 0;  // this lane's pivot, where it holds a new basis row
+    int mypiv = 0;     // this lane's pivot, where it holds a new basis row
     while (pending) {
         uint64_t any = f[0];
 #pragma unroll
         for (int w = 1; w < FW; ++w) any |= f[w];
         const uint64_t nz = __ballot(any != 0) & pending;
-        const int j = nz ? ffs64(nz) : 64;
-        const uint64_t before = (j >= 64) ? pending : (pending & ((1ull << j) - 1));
-        if (before) {
-            const uint64_t cm = __ballot((y0 | y1) != 0) & before;
+        // pending rows before the earliest nonzero one have zero residuals
+        const uint64_t zr = nz ? pending & ((nz & (0ull - nz)) - 1) : pending;
+        if (zr) {
+            const uint64_t cm = __ballot((y0 | y1) != 0) & zr;
             if (cm) {
                 if (ncon == 0) firstc = b0 + ffs64(cm);
                 ncon += __popcll(cm);
             }
-            pending &= ~before;
+            pending &= ~zr;
         }
-        if (j >= 64) break;
+        if (!nz) break;
+        const int j = ffs64(nz);
         uint64_t F[FW];
 #pragma unroll
         for (int w = 0; w < FW; ++w) F[w] = readlane64(f[w], j);
         const uint64_t Y0 = readlane64(y0, j), Y1 = readlane64(y1, j);
-        int p = -1;
+        // pivot: the highest-priority set feature bit, x_{n-1} .. x_0, else the
+        // constant (the row is nonzero)
+        int p = n;
 #pragma unroll
-        for (int w = FW - 1; w >= 0; --w) {
-            const uint64_t v = (w == cw) ? (F[w] & ~cbit) : F[w];
-            if (p < 0 && v) p = 64 * w + msb64(v);
+        for (int w = 0; w < FW; ++w) {
+            const uint64_t v = F[w] & xm[w];
+            p = v ? 64 * w + msb64(v) : p;
         }
-        if (p < 0) p = n;
         const int pw = p >> 6, pb = p & 63;
         const uint32_t mm = bit_mask(sel_word<FW>(f, pw), pb) & (lane == j ? 0u : ~0u);
 #pragma unroll
@@ -844,24 +847,19 @@ __device__ void piv_insert(PivShared& S, int n, int64_t b0, bool valid, uint64_t
         y0 = xor_and(y0, mm, Y0);
         y1 = xor_and(y1, mm, Y1);
         if (lane == j) mypiv = p;
-#pragma unroll
-        for (int w = 0; w < FW; ++w)
-            if (w == pw) npm[w] |= 1ull << pb;
         ins |= 1ull << j;
         pending &= ~(1ull << j);
     }
+    wave_sync();  // npm cleared before the new pivots are added
     if ((ins >> lane) & 1ull) {
         uint64_t* rec = S.rec[mypiv];
 #pragma unroll
         for (int w = 0; w < FW; ++w) rec[w] = f[w];
         rec[FW] = y0;
         rec[FW + 1] = y1;
+        atomicOr(reinterpret_cast<unsigned long long*>(&S.npm[mypiv >> 6]), 1ull << (mypiv & 63));
     }
-    if (lane == 0) {
-#pragma unroll
-        for (int w = 0; w < FW; ++w) S.npm[w] = npm[w];
-        S.nnew = __popcll(ins);
-    }
+    if (lane == 0) S.nnew = __popcll(ins);
 }
 
 // clear the round's new pivots from the retained rows (records of S.pm), one
