@@ -417,9 +417,9 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
         bp[b] = 0;
         piv[b] = 0;
     }
-    uint64_t pm[FW];  // pivot columns (uniform)
+    uint64_t xm[FW];  // the x columns of each feature word (the constant column cleared)
 #pragma unroll
-    for (int w = 0; w < FW; ++w) pm[w] = 0;
+    for (int w = 0; w < FW; ++w) xm[w] = (w == cw) ? ~cbit : ~0ull;
     int rank = 0, ncontra = 0;
     int64_t first = -1;
 
@@ -504,14 +504,14 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
 #pragma unroll
             for (int w = 0; w < FW; ++w) F[w] = readlane64(f[b][w], j);
             const uint64_t Y0 = readlane64(y0[b], j), Y1 = readlane64(y1[b], j);
-            // pivot: highest-priority set feature bit (x_{n-1} .. x_0, then the constant)
-            int p = -1;
+            // pivot: highest-priority set feature bit (x_{n-1} .. x_0, else the
+            // constant: the row is nonzero)
+            int p = n;
 #pragma unroll
-            for (int w = FW - 1; w >= 0; --w) {
-                const uint64_t v = (w == cw) ? (F[w] & ~cbit) : F[w];
-                if (p < 0 && v) p = 64 * w + msb64(v);
+            for (int w = 0; w < FW; ++w) {
+                const uint64_t v = F[w] & xm[w];
+                p = v ? 64 * w + msb64(v) : p;
             }
-            if (p < 0) p = n;
             const int pw = p >> 6, pb = p & 63;
             {  // this block: every row holding bit p except the new basis row itself
                 const uint32_t mm = bit_mask(word_at<FW>(f[b], pw), pb) & (lane == j ? 0u : ~0u);
@@ -531,9 +531,6 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
                 }
             }
             if (lane == j) bp[b] = p;
-#pragma unroll
-            for (int w = 0; w < FW; ++w)
-                if (w == pw) pm[w] |= 1ull << pb;
             piv[b] |= 1ull << j;
             pending &= ~(1ull << j);
             ++rank;
@@ -556,6 +553,9 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
     wave_sync();
     store_mirror(NB, true);
     wave_sync();
+    uint64_t pm[FW];  // pivot columns (uniform): the positions that received a record
+#pragma unroll
+    for (int w = 0; w < FW; ++w) pm[w] = __ballot(64 * w + lane < d && sPos[64 * w + lane] >= 0);
     const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
 #pragma unroll
     for (int k = 0; k < NB; ++k) {
