@@ -2845,13 +2845,16 @@ struct PoolArgs {
     int64_t* row_off;          // [num_pools + 1]: row words per pool, then their offsets
     uint64_t* rows;
     int64_t rows_cap;
+    int64_t* blk;              // [ceil(num_pools / 256) + 1]: words per block of 256 pools, then their
+                               // offsets; last: the total, or -1 when it exceeds rows_cap
 };
 
 constexpr uint32_t kPoolNoRows = F2_POOL_BAD_MEMBER | F2_POOL_WIDTH_MISMATCH;
 
 __global__ __launch_bounds__(256) void k_pool_count(PoolArgs P) {
-    const int p = blockIdx.x * 256 + threadIdx.x;
-    if (p >= P.num_pools) return;
+    const int p0 = blockIdx.x * 256 + threadIdx.x;
+    const bool live = p0 < P.num_pools;
+    const int p = live ? p0 : P.num_pools - 1;  // lanes past the end redo the last pool and store nothing
     const int64_t lo = P.pool_off[p], hi = P.pool_off[p + 1];
     const int n = P.pooled_n[p];
     const int64_t W = feat_words(n < 0 ? 0 : n) + F2_Y_WORDS;
@@ -2876,56 +2879,126 @@ __global__ __launch_bounds__(256) void k_pool_count(PoolArgs P) {
         }
         words += static_cast<int64_t>(P.rank[c]) * W;
     }
-    P.pool_flags[p] = fl;
-    P.row_off[p] = (fl & kPoolNoRows) ? 0 : words;
+    if (live) {
+        P.pool_flags[p] = fl;
+        P.row_off[p] = (fl & kPoolNoRows) ? 0 : words;
+    }
+    // the block's words
+    __shared__ int64_t sSum[4];
+    int64_t v = (!live || (fl & kPoolNoRows)) ? 0 : words;
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o);
+    if ((threadIdx.x & 63) == 0) sSum[threadIdx.x >> 6] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t t = 0;
+        for (int w = 0; w < 4; ++w) t += sSum[w];
+        P.blk[blockIdx.x] = t;
+    }
 }
 
-// one workgroup: exclusive scan of the row words; a total beyond the buffer (a
-// context in several pools) empties every pool and flags it
+// one workgroup: exclusive scan of the blocks' words (1024 blocks at a time,
+// coalesced); the last entry gets the total, or -1 beyond the buffer (a context
+// in several pools), which empties every pool and flags it
 __global__ __launch_bounds__(1024) void k_pool_scan(PoolArgs P) {
     __shared__ int64_t sWave[16];
     const int tid = threadIdx.x, lane = tid & 63;
-    const int per = (P.num_pools + 1023) / 1024;
-    const int p0 = tid * per;
-    int64_t sum = 0;
-    for (int k = 0; k < per; ++k)
-        if (p0 + k < P.num_pools) sum += P.row_off[p0 + k];
-    int64_t x = sum;
+    const int nblk = (P.num_pools + 255) / 256;
+    int64_t carry = 0;
+    for (int b0 = 0; b0 < nblk; b0 += 1024) {
+        const int b = b0 + tid;
+        const int64_t v = b < nblk ? P.blk[b] : 0;
+        int64_t x = v;
+        for (int o = 1; o < 64; o <<= 1) {
+            const int64_t t = __shfl_up(x, o);
+            if (lane >= o) x += t;
+        }
+        if (lane == 63) sWave[tid >> 6] = x;
+        __syncthreads();
+        int64_t run = x - v, total = 0;
+        for (int w = 0; w < 16; ++w) {
+            total += sWave[w];
+            if (w < (tid >> 6)) run += sWave[w];
+        }
+        if (b < nblk) P.blk[b] = carry + run;
+        carry += total;
+        __syncthreads();  // sWave is rewritten by the next chunk
+    }
+    if (tid == 0) P.blk[nblk] = carry > P.rows_cap ? -1 : carry;
+}
+
+// the pools' row offsets: their block's offset plus the scan within the block
+__global__ __launch_bounds__(256) void k_pool_offsets(PoolArgs P) {
+    __shared__ int64_t sWave[4];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int p = blockIdx.x * 256 + tid;
+    const int nblk = (P.num_pools + 255) / 256;
+    const bool live = p < P.num_pools;
+    const int64_t v = live ? P.row_off[p] : 0;
+    const int64_t total = P.blk[nblk], base = P.blk[blockIdx.x];
+    int64_t x = v;
     for (int o = 1; o < 64; o <<= 1) {
         const int64_t t = __shfl_up(x, o);
         if (lane >= o) x += t;
     }
     if (lane == 63) sWave[tid >> 6] = x;
     __syncthreads();
-    int64_t run = x - sum, total = 0;
-    for (int w = 0; w < 16; ++w) {
-        total += sWave[w];
-        if (w < (tid >> 6)) run += sWave[w];
+    int64_t run = base + x - v;
+    for (int w = 0; w < (tid >> 6); ++w) run += sWave[w];
+    const bool over = total < 0;
+    if (live) {
+        P.row_off[p] = over ? 0 : run;
+        if (over) P.pool_flags[p] |= F2_POOL_BAD_MEMBER;
     }
-    const bool over = total > P.rows_cap;
-    for (int k = 0; k < per; ++k)
-        if (p0 + k < P.num_pools) {
-            const int64_t v = P.row_off[p0 + k];
-            P.row_off[p0 + k] = over ? 0 : run;
-            if (over) P.pool_flags[p0 + k] |= F2_POOL_BAD_MEMBER;
-            run += v;
-        }
-    if (tid == 0) P.row_off[P.num_pools] = over ? 0 : total;
+    if (p == P.num_pools - 1) P.row_off[P.num_pools] = over ? 0 : total;
 }
 
-// one workgroup per pool: the members' basis rows, in member order, each in its stored order
+// one wavefront per pool: the members' basis rows, in member order, each in its
+// stored order.  Up to 64 members at a time, one per lane (their ranks and
+// offsets loaded together); every lane then copies words of the group's output,
+// the member of each word found among the lanes' prefixes.
 __global__ __launch_bounds__(256) void k_pool_copy(PoolArgs P) {
-    const int p = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (p >= P.num_pools) return;
     if (P.pool_flags[p] & kPoolNoRows) return;
     const int64_t lo = P.pool_off[p], hi = P.pool_off[p + 1];
     const int64_t W = feat_words(P.pooled_n[p]) + F2_Y_WORDS;
     int64_t dst = P.row_off[p];
-    for (int64_t e = lo; e < hi; ++e) {
-        const int c = P.members[e];
-        const int64_t words = static_cast<int64_t>(P.rank[c]) * W;
-        const uint64_t* src = P.basis + P.basis_off[c];
-        for (int64_t k = threadIdx.x; k < words; k += 256) P.rows[dst + k] = src[k];
-        dst += words;
+    for (int64_t e0 = lo; e0 < hi; e0 += 64) {
+        const int64_t e = e0 + lane;
+        int64_t words = 0, src = 0;
+        if (e < hi) {
+            const int c = P.members[e];
+            words = static_cast<int64_t>(P.rank[c]) * W;
+            src = P.basis_off[c];
+        }
+        int64_t x = words;  // inclusive prefix over the group's members
+        for (int o = 1; o < 64; o <<= 1) {
+            const int64_t t = __shfl_up(x, o);
+            if (lane >= o) x += t;
+        }
+        const int64_t pre = x - words;
+        const int64_t total = __shfl(x, 63);
+        const int nm = hi - e0 < 64 ? static_cast<int>(hi - e0) : 64;
+        for (int64_t k = lane; k < total; k += 64) {
+            // the member holding output word k: the last with prefix <= k (its prefix
+            // and source offset read from its lane by readlane, which, unlike a
+            // permute, also reads lanes this loop has left inactive)
+            int64_t ps = 0;
+            int64_t ss = (static_cast<int64_t>(__builtin_amdgcn_readlane(static_cast<int32_t>(src >> 32), 0)) << 32) |
+                         (static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int32_t>(src), 0)));
+            for (int i = 1; i < nm; ++i) {
+                const int64_t pi = (static_cast<int64_t>(__builtin_amdgcn_readlane(static_cast<int32_t>(pre >> 32), i)) << 32) |
+                                   (static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int32_t>(pre), i)));
+                if (k >= pi) {
+                    ps = pi;
+                    ss = (static_cast<int64_t>(__builtin_amdgcn_readlane(static_cast<int32_t>(src >> 32), i)) << 32) |
+                         (static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int32_t>(src), i)));
+                }
+            }
+            P.rows[dst + k] = P.basis[ss + (k - ps)];
+        }
+        dst += total;
     }
 }
 
@@ -3259,6 +3332,7 @@ size_t f2_pool_workspace_bytes(const f2_model* members_model, int32_t num_pools)
     if (!members_model || members_model->basis_words < 0 || num_pools < 0) return 0;
     return align256(sizeof(int64_t) * (static_cast<size_t>(num_pools) + 1)) +
            align256(sizeof(uint64_t) * static_cast<size_t>(members_model->basis_words)) +
+           align256(sizeof(int64_t) * (static_cast<size_t>((num_pools + 255) / 256) + 1)) +
            f2_fit_workspace_bytes(num_pools);
 }
 
@@ -3297,11 +3371,14 @@ int f2_pool_bases(const f2_model* members_model, const uint64_t* out_mask, const
     const size_t off_rows = align256(sizeof(int64_t) * (static_cast<size_t>(P) + 1));
     A.rows = reinterpret_cast<uint64_t*>(ws + off_rows);
     A.rows_cap = members_model->basis_words;
-    int32_t* plan = reinterpret_cast<int32_t*>(ws + off_rows + align256(sizeof(uint64_t) * A.rows_cap));
+    const size_t off_blk = off_rows + align256(sizeof(uint64_t) * A.rows_cap);
     const unsigned pb = static_cast<unsigned>((P + 255) / 256);
+    A.blk = reinterpret_cast<int64_t*>(ws + off_blk);
+    int32_t* plan = reinterpret_cast<int32_t*>(ws + off_blk + align256(sizeof(int64_t) * (static_cast<size_t>(pb) + 1)));
     hipLaunchKernelGGL(k_pool_count, dim3(pb), dim3(256), 0, s, A);
     hipLaunchKernelGGL(k_pool_scan, dim3(1), dim3(1024), 0, s, A);
-    hipLaunchKernelGGL(k_pool_copy, dim3(static_cast<unsigned>(P)), dim3(256), 0, s, A);
+    hipLaunchKernelGGL(k_pool_offsets, dim3(pb), dim3(256), 0, s, A);
+    hipLaunchKernelGGL(k_pool_copy, dim3(static_cast<unsigned>((P + 3) / 4)), dim3(256), 0, s, A);
     launch_fit(fit_args(A.rows, A.rows_cap, A.row_off, pooled, plan), s);
     hipLaunchKernelGGL(k_pool_finish, dim3(pb), dim3(256), 0, s, A);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;

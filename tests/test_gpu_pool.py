@@ -131,4 +131,26 @@ def test_pool_flags_masks_bad_members_and_overflow(f2):
     assert (got == PL.POOL_BAD_MEMBER).all() and (parity.host(pooled.rank, np.int32)[:6] == 0).all()
 
 
+def test_pool_many_members_per_pool(f2):
+    """Pools of 70 to 150 members (more than the 64 members the copy takes at a time),
+    each the shards of one long recipe-3 context, against the pooling oracle."""
+    wl0 = synth.fit_workload(3, num_ctx=20000)
+    long_ctx = [c for c in range(wl0.num_ctx) if wl0.m_rows[c] >= 300][:24]
+    assert len(long_ctx) == 24
+    rng = np.random.default_rng(13)
+    n_bits, rows_list, pool_off, pooled_n = [], [], [0], []
+    for c in long_ctx:
+        n = int(wl0.n_bits[c]); W = (n + 64) // 64 + 2
+        rows = wl0.rows[wl0.row_off[c]:wl0.row_off[c + 1]].reshape(-1, W)
+        k = int(rng.integers(70, 151))
+        for part in np.array_split(rows, k):
+            n_bits.append(n)
+            rows_list.append(part)
+        pool_off.append(pool_off[-1] + k)
+        pooled_n.append(n)
+    wl = synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+    exp = _pool_and_compare(f2, wl, np.asarray(pool_off, np.int64), np.arange(wl.num_ctx), pooled_n)
+    assert (exp.flags != PL.POOL_BAD_MEMBER).sum() > 12
+
+
 ALLW = 2 ** 64 - 1
