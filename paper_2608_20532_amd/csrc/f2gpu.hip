@@ -116,10 +116,11 @@ struct CtxDesc {
     int c, n;
     uint32_t bad;
     int64_t row0, m;
+    int64_t bo, po, mo;  // output offsets: basis (and parity rows), pivots, map
 };
 
 __device__ __forceinline__ CtxDesc load_desc(const FitArgs& a, int64_t c) {
-    CtxDesc ds{-1, -1, 0u, 0, 0};  // c = -1: no context
+    CtxDesc ds{-1, -1, 0u, 0, 0, 0, 0, 0};  // c = -1: no context
     if (c >= a.num_ctx) return ds;
     ds.c = static_cast<int>(c);
     // every load first (one memory latency), then the checks in order
@@ -127,6 +128,9 @@ __device__ __forceinline__ CtxDesc load_desc(const FitArgs& a, int64_t c) {
     const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
     const int64_t s0 = a.row_off[c], s1 = a.row_off[c + 1];
     ds.n = n;
+    ds.bo = bo;
+    ds.po = po;
+    ds.mo = mo;
     if (n < 0 || n > F2_MAX_N_BITS || (a.max_n >= 0 && n > a.max_n)) {  // outside the supported or declared range
         ds.bad = F2_CTX_BAD_WIDTH;
         return ds;
@@ -154,6 +158,9 @@ __device__ __forceinline__ CtxDesc readlane_desc(const CtxDesc& v, int t) {
     ds.bad = __builtin_amdgcn_readlane(v.bad, t);
     ds.row0 = static_cast<int64_t>(readlane64(static_cast<uint64_t>(v.row0), t));
     ds.m = static_cast<int64_t>(readlane64(static_cast<uint64_t>(v.m), t));
+    ds.bo = static_cast<int64_t>(readlane64(static_cast<uint64_t>(v.bo), t));
+    ds.po = static_cast<int64_t>(readlane64(static_cast<uint64_t>(v.po), t));
+    ds.mo = static_cast<int64_t>(readlane64(static_cast<uint64_t>(v.mo), t));
     return ds;
 }
 
@@ -556,7 +563,7 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
     uint64_t pm[FW];  // pivot columns (uniform): the positions that received a record
 #pragma unroll
     for (int w = 0; w < FW; ++w) pm[w] = __ballot(64 * w + lane < d && sPos[64 * w + lane] >= 0);
-    const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
+    const int64_t bo = ds.bo, po = ds.po, mo = ds.mo;
 #pragma unroll
     for (int k = 0; k < NB; ++k) {
         if ((piv[k] >> lane) & 1ull) {
@@ -637,19 +644,32 @@ __global__ __launch_bounds__(64 * kRegWaves) void k_fit_reg(FitArgs a) {
     if (tid == 0) sNext = kRegWaves;
     __syncthreads();
     const int r = wave >> 2, simd = wave & 3;
-    int k = 4 * r + ((r & 1) ? 3 - simd : simd);
-    for (;;) {
-        const int c = __builtin_amdgcn_readfirstlane(class_ctx(a, kClsReg, k));
-        if (c < 0) break;
-        const CtxDesc ds = readlane_desc(load_desc(a, c), 0);
+    // the share's list positions (the class bounds read once)
+    const int lo = a.plan[kClsReg], cnt = a.plan[kClsReg + 1] - lo;
+    const int G = static_cast<int>(gridDim.x), g = static_cast<int>(blockIdx.x);
+    auto ctx_at = [&](int i) {  // context at position i of the share, or num_ctx past its end
+        const int64_t e = static_cast<int64_t>(i) * G + ((i & 1) ? G - 1 - g : g);
+        return __builtin_amdgcn_readfirstlane(e < cnt ? a.plan[kPlanHead + lo + static_cast<int>(e)] : a.num_ctx);
+    };
+    auto next_pos = [&]() {
+        int nk = 0;
+        if (lane == 0) nk = atomicAdd(&sNext, 1);
+        return __builtin_amdgcn_readfirstlane(nk);
+    };
+    // a two-deep pipeline: while a context is fitted, the next one's descriptor
+    // and the one after's id are already loading
+    CtxDesc ds = readlane_desc(load_desc(a, ctx_at(4 * r + ((r & 1) ? 3 - simd : simd))), 0);
+    int c1 = ctx_at(next_pos());
+    while (ds.c >= 0) {
+        const CtxDesc dn = readlane_desc(load_desc(a, c1), 0);
+        const int c2 = ctx_at(next_pos());
         switch (feat_words(ds.n)) {
             case 1: fit_ctx_reg<1>(a, ds, sRec[wave], sPos[wave]); break;
             case 2: fit_ctx_reg<2>(a, ds, sRec[wave], sPos[wave]); break;
             default: fit_ctx_reg<3>(a, ds, sRec[wave], sPos[wave]); break;
         }
-        int nk = 0;
-        if (lane == 0) nk = atomicAdd(&sNext, 1);
-        k = __builtin_amdgcn_readfirstlane(nk);
+        ds = dn;
+        c1 = c2;
     }
 }
 
@@ -1009,7 +1029,7 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
     __syncthreads();
 
     // outputs: basis rows and pivots in descending priority, canonical map, encode table, scalars
-    const int64_t bo = a.basis_off[c], po = a.piv_off[c], mo = a.map_off[c];
+    const int64_t bo = ds.bo, po = ds.po, mo = ds.mo;
     const int cw = n >> 6;
     const uint64_t cbit = 1ull << (n & 63);
     for (int j = tid; j < d; j += 64 * NW) {
