@@ -237,6 +237,48 @@ def test_fit_declared_width_bound(f2):
             assert np.array_equal(g["basis"][bo:bo + r * W], ref.basis[bo:bo + r * W]), f"basis of context {c}"
 
 
+@pytest.mark.parametrize("num_ctx", [40, 1000, 5000])
+def test_fit_invalid_contexts_each_launch_path(f2, num_ctx):
+    """Invalid contexts among valid ones under a declared width bound below 512: the
+    one-launch path of small batches (40 contexts) and the planned class kernels (1000,
+    5000).  A width above the bound, two malformed segments and output offsets past the
+    buffers are flagged with rank 0; every other context matches the oracle's fit of
+    the unmodified batch."""
+    import torch
+    from paper_2608_20532_amd import f2gpu
+    wl = synth.fit_workload(2, num_ctx=num_ctx)
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    n_bits = wl.n_bits.copy()
+    row_off = wl.row_off.copy()
+    n_bits[1] = 300                 # above the declared bound
+    row_off[4] += 1                 # segments 3 and 4 no longer whole rows
+    model = f2gpu.Model(n_bits, max_n_bits=127)
+    bo = model.basis_off_host.copy()
+    bo[6] = int(bo[-1])             # basis past the buffer
+    model.basis_off = parity.to_dev(bo)
+    model._struct = None
+    nb = f2gpu.f2_fit_workspace_bytes(model.num_ctx)
+    ws = f2gpu.workspace(nb)
+    assert f2gpu.f2_fit_batch(parity.to_dev(wl.rows), wl.rows.size, parity.to_dev(row_off), model, ws, nb) == 0
+    torch.cuda.synchronize()
+    g = parity.model_to_host(model)
+    assert g["flags"][1] == oracle.CTX_BAD_WIDTH
+    assert g["flags"][3] == oracle.CTX_BAD_SEGMENT and g["flags"][4] == oracle.CTX_BAD_SEGMENT
+    assert g["flags"][6] == oracle.CTX_BAD_OUTPUT
+    bad = np.zeros(num_ctx, bool)
+    bad[[1, 3, 4, 6]] = True
+    assert not g["rank"][bad].any()
+    ok = ~bad
+    for k, r in (("flags", ref.flags), ("rank", ref.rank), ("n_contra", ref.n_contra), ("first", ref.first_contra)):
+        assert np.array_equal(g[k][ok], r[ok]), k
+    rb = ref.basis_off
+    for c in np.nonzero(ok)[0][:300]:
+        d, W, r = int(wl.n_bits[c]) + 1, (int(wl.n_bits[c]) + 64) // 64 + 2, int(ref.rank[c])
+        assert np.array_equal(g["basis"][int(bo[c]):int(bo[c]) + r * W], ref.basis[int(rb[c]):int(rb[c]) + r * W]), c
+        mo, rmo = int(model.map_off_host[c]), int(ref.map_off[c])
+        assert np.array_equal(g["maps"][mo:mo + 2 * d], ref.maps[rmo:rmo + 2 * d]), c
+
+
 def test_fit_host_errors(f2):
     from paper_2608_20532_amd import f2gpu
     wl = synth.fit_workload(1)
