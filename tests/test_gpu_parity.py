@@ -378,14 +378,16 @@ def test_encode_recipe5_full_size_sampled(f2):
     assert 0.008 < planted.mean() < 0.012
 
 
-def test_encode_grouped_path_random_widths(f2):
-    """A batch large enough for the context-grouped encode, with every context class and bad ids mixed in."""
+@pytest.mark.parametrize("stride", [3, 1, 7])
+def test_encode_grouped_path_random_widths(f2, stride):
+    """A batch large enough for the context-grouped encode, with every context class and
+    bad ids mixed in; strides of 1 word (x read a word at a time), 3, and 7 (words past
+    the first four checked for bits outside the width)."""
     rng = np.random.default_rng(21)
     widths = list(rng.integers(0, 190, size=300)) + list(rng.integers(190, 600, size=30)) + [0, 63, 64, 4095]
     wl = _random_batch(23, widths, max_rows=100)
     ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
     model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
-    stride = 3
     nq = 200_000   # grouped from 196,608 queries (and 4 per context) on
     ctx = rng.integers(-3, wl.num_ctx + 3, size=nq).astype(np.int32)
     x = np.zeros((nq, stride), np.uint64)
