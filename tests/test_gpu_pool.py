@@ -153,4 +153,28 @@ def test_pool_many_members_per_pool(f2):
     assert (exp.flags != PL.POOL_BAD_MEMBER).sum() > 12
 
 
+def test_pool_more_than_a_thousand_offset_blocks(f2):
+    """270,000 pools (the row-offset scan runs over 1,055 blocks of 256 pools, more than
+    one chunk of 1,024), each the two halves of a small consistent context: every pool
+    is shared and its fit equals the oracle's fit of the whole context."""
+    import torch
+    rng = np.random.default_rng(17)
+    P, n, m = 270_000, 12, 4
+    X = rng.integers(0, 1 << n, size=(P, m), dtype=np.uint64) | (np.uint64(1) << np.uint64(n))
+    Wm = rng.integers(0, 2 ** 63, size=(P, n + 1, 2), dtype=np.uint64)
+    Y = np.zeros((P, m, 2), np.uint64)
+    for b in range(n + 1):  # y = W phi over GF(2): consistent, no contradiction
+        sel = ((X >> np.uint64(b)) & np.uint64(1)).astype(bool)
+        Y ^= np.where(sel[:, :, None], Wm[:, b][:, None, :], np.uint64(0))
+    rows = np.ascontiguousarray(np.concatenate([X[:, :, None], Y], axis=2)).reshape(-1)  # P contexts of m rows
+    W = 3                                                                # words per row (n < 63)
+    # the members: each context's two halves, consecutive segments of the same rows
+    model = parity.gpu_fit(f2, rows, np.arange(2 * P + 1, dtype=np.int64) * (m // 2) * W, np.full(2 * P, n, np.int32))
+    pooled, flags = f2.pool(model, parity.to_dev(np.arange(0, 2 * P + 1, 2, dtype=np.int64)),
+                            parity.to_dev(np.arange(2 * P, dtype=np.int32)), np.full(P, n, np.int32))
+    torch.cuda.synchronize()
+    assert (parity.host(flags, np.uint32)[:P] == PL.POOL_SHARED).all()
+    parity.compare_fit(pooled, oracle.fit_batch(rows, np.arange(P + 1, dtype=np.int64) * m * W, np.full(P, n, np.int32)))
+
+
 ALLW = 2 ** 64 - 1
