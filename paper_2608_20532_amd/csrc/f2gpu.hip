@@ -2039,11 +2039,11 @@ __device__ __forceinline__ bool basis_scan(const uint64_t* B, const int32_t* piv
             z1 ^= rv[5] & mk;
         };
         int k = 0;
-        for (; k + 4 <= rank; k += 4) {  // four rows in flight
-            int p[4];
-            uint64_t rv[4][6];
+        for (; k + 2 <= rank; k += 2) {  // two rows in flight (four cost a third of the occupancy of the per-lane passes)
+            int p[2];
+            uint64_t rv[2][6];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < 2; ++u) {
                 p[u] = piv[k + u];
                 const uint64_t* row = B + static_cast<int64_t>(k + u) * W;
 #pragma unroll
@@ -2052,7 +2052,7 @@ __device__ __forceinline__ bool basis_scan(const uint64_t* B, const int32_t* piv
                 rv[u][5] = row[fw + 1];
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) add_row(p[u], rv[u]);
+            for (int u = 0; u < 2; ++u) add_row(p[u], rv[u]);
         }
         for (; k < rank; ++k) {
             const uint64_t* row = B + static_cast<int64_t>(k) * W;
