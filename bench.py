@@ -338,8 +338,8 @@ def main():
                     help="only run a plain device-to-device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: contexts are independent and would shard across GPUs with no "
-              "exchange, but this build runs and reports a single GPU only; use --gpus 1", file=sys.stderr)
+        print("bench.py runs and reports one GPU only (contexts are independent and would shard across "
+              "GPUs with no exchange); use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
