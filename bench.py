@@ -57,6 +57,8 @@ STREAM_WORKLOADS = {
                               "restored from recorded state"),
     "pool": (80_000, 3, "pool the bases of 240,000 shard contexts (each n-in-[8,256] context's rows split in 3, "
                         "fitted apart) back into 80,000 contexts"),
+    "group": (7_240_070, 0, "group the 7,240,070 rows of the n-in-[8,256] fit workload, interleaved at random "
+                            "(each context's order kept, stride 7 words), back by context for the fit"),
 }
 
 
@@ -327,6 +329,80 @@ def bench_pool(args):
     }), flush=True)
 
 
+def bench_group(args):
+    """Time f2_group_rows: the rows of the 80,000-context fit workload interleaved at
+    random (each context's order kept), grouped back by context."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2608_20532_amd import f2gpu
+    _, _, desc = STREAM_WORKLOADS["group"]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(0)
+    wl = synth.fit_workload(3)
+    W = (wl.n_bits.astype(np.int64) + 64) // 64 + 2
+    S = int(W.max())
+    rng = np.random.default_rng(0xF2A50006)
+    ids = np.repeat(np.arange(wl.num_ctx, dtype=np.int32), wl.m_rows)
+    ids = ids[rng.permutation(len(ids))]
+    start = np.concatenate([[0], np.cumsum(wl.m_rows)[:-1]])
+    order = np.argsort(ids, kind="stable")
+    rank = np.empty(len(ids), np.int64)
+    rank[order] = np.arange(len(ids)) - start[ids[order]]
+    rows = np.zeros((len(ids), S), np.uint64)
+    src = wl.row_off[ids] + rank * W[ids]
+    for w in range(S):
+        ok = w < W[ids]
+        rows[ok, w] = wl.rows[src[ok] + w]
+    R, C = len(ids), wl.num_ctx
+    to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int64) if a.dtype == np.uint64 else a).to(dev)
+    ids_d, rows_d, nb_d = to_dev(ids), to_dev(rows.reshape(-1)), to_dev(wl.n_bits.astype(np.int32))
+    out = torch.empty(R * S, dtype=torch.int64, device=dev)
+    off = torch.empty(C + 1, dtype=torch.int64, device=dev)
+    drop = torch.empty(1, dtype=torch.int64, device=dev)
+    nb = f2gpu.f2_group_workspace_bytes(C, R)
+    ws = f2gpu.workspace(nb, dev)
+    stream = torch.cuda.current_stream()
+    call = lambda: f2gpu.f2_group_rows(ids_d, rows_d, S, R, nb_d, C, out, R * S, off, drop, ws, nb,
+                                       stream.cuda_stream)
+    for _ in range(args.warmup):
+        assert call() == 0
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    w0 = time.perf_counter()
+    for e in ev:
+        e[0].record(stream)
+        assert call() == 0
+        e[1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    assert np.array_equal(off.cpu().numpy(), wl.row_off)
+    # algorithmic bytes: each row's id and its fw + 2 words read, the words written, the offsets
+    nbytes = int(4 * R + 16 * int((W * wl.m_rows).sum()) + 8 * (C + 1))
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import group as G
+        k = min(R, 400_000)
+        t0 = time.perf_counter()
+        G.group_rows(ids[:k], rows[:k], S, wl.n_bits)
+        cpu = {"value": k / (time.perf_counter() - t0), "unit": "rows/s", "cores": 1, "kind": "oracle",
+               "sample": f"oracle grouping of the first {k} rows of the stream"}
+    print(json.dumps({
+        "metric": "GF(2) fit rows/sec and encoded words/sec on 1 MI355X; % of HBM/int-op roofline",
+        "value": R / (ms * 1e-3), "unit": "rows/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": 1e3 * wall / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": desc, "name": "group", "rows": R, "contexts": C, "stride_words": S},
+        "roofline": measured_traffic("group", "group",
+                                     {"bound": "hbm", "kernel": "f2_group_rows", "achieved": gbps, "peak": HBM_PEAK_GBS,
+                                      "unit": "GB/s", "frac": gbps / HBM_PEAK_GBS, "algorithmic_bytes": nbytes,
+                                      "avg_ms": ms}),
+        "cpu_baseline": cpu,
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -357,6 +433,9 @@ def main():
         print(json.dumps({"copy_calibration_bytes": nbytes, "copies": 3}), flush=True)
         return
 
+    if args.workload == "group":
+        bench_group(args)
+        return
     if args.workload == "pool":
         bench_pool(args)
         return

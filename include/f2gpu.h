@@ -242,6 +242,31 @@ int f2_pool_bases(const f2_model* members_model, const uint64_t* out_mask, const
                   const int32_t* members, int64_t num_members, const f2_model* pooled, uint32_t* pool_flags,
                   void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Interleaved-stream ingestion: group a stream of fit rows of many contexts,
+ * mixed in stream order (observations gathered across a corpus, Sec. 3), by
+ * context, keeping each context's rows in stream order (the kept-row semantics
+ * of the streaming elimination, Sec. 2.2, depend on it).
+ *   ctx_id      [num_rows] context of each row
+ *   rows        [num_rows * row_stride_words] each row in the packed layout of
+ *               its context (fw + 2 words, see the top of this file) at the
+ *               start of its stride; the words past fw + 2 are ignored
+ *   n_bits      [num_ctx] width of each context
+ *   rows_out    [rows_out_words >= num_rows * row_stride_words] the grouped
+ *               rows, trimmed to fw + 2 words: a valid f2_fit_batch input
+ *   row_off_out [num_ctx + 1] word offsets of each context's rows in rows_out
+ *               (f2_fit_batch's row_off)
+ *   dropped_out [1] rows dropped: context id out of range, context width
+ *               outside [0, F2_MAX_N_BITS], or fw + 2 above the stride
+ *   workspace   f2_group_workspace_bytes(num_ctx, num_rows) bytes, 256-byte aligned
+ * Returns F2_OK, F2_EINVAL (also for num_rows above 2^31 - 1 or a stride below
+ * 3 words), F2_EWORKSPACE or F2_EDEVICE.
+ */
+size_t f2_group_workspace_bytes(int32_t num_ctx, int64_t num_rows);
+int f2_group_rows(const int32_t* ctx_id, const uint64_t* rows, int32_t row_stride_words, int64_t num_rows,
+                  const int32_t* n_bits, int32_t num_ctx, uint64_t* rows_out, int64_t rows_out_words,
+                  int64_t* row_off_out, int64_t* dropped_out, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* f2_status_string(int status);
 

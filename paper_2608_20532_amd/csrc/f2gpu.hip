@@ -3048,7 +3048,267 @@ __global__ __launch_bounds__(256) void k_pool_finish(PoolArgs P) {
     P.pool_flags[p] = fl ? fl : F2_POOL_SHARED;
 }
 
+
+// ---------------------------------------------------------------------------
+// interleaved-stream ingestion: the rows of many contexts arrive mixed, in
+// stream order (Sec. 3: observations are gathered across a corpus); the fit takes
+// each context's rows contiguous and in stream order.  A stable LSD radix sort of
+// (context, row) pairs by context, 8 bits per pass (per-block LDS histograms, the
+// column scan of the encode sort, a stable scatter), then each context's rows are
+// copied, trimmed to its row width, to their offsets.  Rows of an out-of-range
+// context, of a width outside [0, F2_MAX_N_BITS], or wider than the stride sort
+// last and are dropped.
+// ---------------------------------------------------------------------------
+constexpr int kGrpBins = 256;
+constexpr int kGrpThreads = 1024;
+constexpr int kGrpWaves = kGrpThreads / 64;
+
+struct GroupArgs {
+    int32_t num_ctx;
+    const int32_t* n_bits;
+    const int32_t* ctx_id;
+    const uint64_t* rows;
+    int32_t stride;
+    int64_t nr;             // rows
+    int32_t blocks;
+    int64_t qc;             // rows per count / scatter block
+    int32_t shift;          // digit of this pass: (key >> shift) & 255
+    const int2* in;         // pairs (key, row) of the previous pass, or null (first pass: from ctx_id)
+    int2* out;
+    int32_t* hist;          // [blocks][kGrpBins]
+    int32_t* total;         // [kGrpBins]
+    int32_t* first;         // [num_ctx] first sorted position of each context
+    int32_t* count;         // [num_ctx] rows of each context
+    int64_t* blk;           // [ceil(num_ctx / 1024) + 1] words per block of contexts, then their offsets
+    uint64_t* rows_out;
+    int64_t* row_off;       // [num_ctx + 1]
+    int64_t* dropped;       // [1]
+};
+
+// the sort key of a row: its context, or num_ctx for a row that is dropped
+__device__ __forceinline__ int group_key(const GroupArgs& g, int64_t r) {
+    const int c = g.ctx_id[r];
+    if (c < 0 || c >= g.num_ctx) return g.num_ctx;
+    const int n = g.n_bits[c];
+    if (n < 0 || n > F2_MAX_N_BITS || feat_words(n) + F2_Y_WORDS > g.stride) return g.num_ctx;
+    return c;
+}
+
+__device__ __forceinline__ int2 group_pair(const GroupArgs& g, int64_t r) {
+    return g.in ? g.in[r] : make_int2(group_key(g, r), static_cast<int>(r));
+}
+
+__global__ __launch_bounds__(kGrpThreads) void k_grp_count(GroupArgs g) {
+    __shared__ int sBin[kGrpBins];
+    const int tid = threadIdx.x;
+    if (tid < kGrpBins) sBin[tid] = 0;
+    __syncthreads();
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * g.qc;
+    const int64_t r1 = r0 + g.qc < g.nr ? r0 + g.qc : g.nr;
+    for (int64_t r = r0 + tid; r < r1; r += kGrpThreads)
+        atomicAdd(&sBin[(group_pair(g, r).x >> g.shift) & (kGrpBins - 1)], 1);
+    __syncthreads();
+    if (tid < kGrpBins) g.hist[static_cast<int64_t>(blockIdx.x) * kGrpBins + tid] = sBin[tid];
+}
+
+// stable scatter: the block's rows in rounds of kGrpThreads, wavefront w taking
+// the round's w-th 64 rows; within a wavefront a row's rank among equal digits
+// comes from the ballots of the digit bits, across wavefronts from per-wavefront
+// digit counts, across rounds from the running cursor of each digit
+__global__ __launch_bounds__(kGrpThreads) void k_grp_scatter(GroupArgs g) {
+    __shared__ int sCur[kGrpBins];
+    __shared__ int sCnt[kGrpWaves][kGrpBins];
+    __shared__ int sBase[kGrpBins];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid < kGrpBins) {  // the bin's start: bins before it over every block, then the blocks before this one
+        int base = 0;
+        for (int b = 0; b < tid; ++b) base += g.total[b];
+        sCur[tid] = base + g.hist[static_cast<int64_t>(blockIdx.x) * kGrpBins + tid];
+    }
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * g.qc;
+    const int64_t r1 = r0 + g.qc < g.nr ? r0 + g.qc : g.nr;
+    const uint64_t lt = (1ull << lane) - 1;
+    for (int64_t rb = r0; rb < r1; rb += kGrpThreads) {
+        for (int k = tid; k < kGrpWaves * kGrpBins; k += kGrpThreads) (&sCnt[0][0])[k] = 0;
+        const int64_t r = rb + 64 * wave + lane;
+        const bool live = r < r1;
+        const int2 pr = live ? group_pair(g, r) : make_int2(0, 0);
+        const int dg = (pr.x >> g.shift) & (kGrpBins - 1);
+        uint64_t peers = __ballot(live);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const uint64_t m = __ballot(live && ((dg >> b) & 1));
+            peers &= ((dg >> b) & 1) ? m : ~m;
+        }
+        const int rank = __popcll(peers & lt);
+        __syncthreads();  // counts cleared
+        if (live && rank == __popcll(peers) - 1) sCnt[wave][dg] = __popcll(peers);  // the group's last lane
+        __syncthreads();
+        if (tid < kGrpBins) {  // per digit: exclusive prefix over the wavefronts, the round's count to the cursor
+            int run = sCur[tid];
+            for (int w = 0; w < kGrpWaves; ++w) {
+                const int c = sCnt[w][tid];
+                sCnt[w][tid] = run;
+                run += c;
+            }
+            sBase[tid] = run;
+        }
+        __syncthreads();
+        if (live) g.out[sCnt[wave][dg] + rank] = pr;
+        __syncthreads();
+        if (tid < kGrpBins) sCur[tid] = sBase[tid];
+    }
+}
+
+// first position and row count of each context, rows dropped (contexts zeroed first)
+__global__ __launch_bounds__(256) void k_grp_clear(GroupArgs g) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    if (c < g.num_ctx) {
+        g.first[c] = 0;
+        g.count[c] = 0;
+    }
+    if (c == 0) *g.dropped = 0;
+}
+
+__global__ __launch_bounds__(256) void k_grp_bounds(GroupArgs g) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= g.nr) return;
+    const int k = g.in[i].x;
+    const bool start = i == 0 || g.in[i - 1].x != k;
+    if (k == g.num_ctx) {
+        if (start) *g.dropped = g.nr - i;
+        return;
+    }
+    if (start) g.first[k] = static_cast<int32_t>(i);
+    if (i == g.nr - 1 || g.in[i + 1].x != k) g.count[k] = static_cast<int32_t>(i + 1);  // end, made a count below
+}
+
+// words per block of 1024 contexts (end positions made counts)
+__global__ __launch_bounds__(1024) void k_grp_words(GroupArgs g) {
+    __shared__ int64_t sW[16];
+    const int c = blockIdx.x * 1024 + threadIdx.x;
+    int64_t v = 0;
+    if (c < g.num_ctx) {
+        const int cnt = g.count[c] ? g.count[c] - g.first[c] : 0;
+        g.count[c] = cnt;
+        v = static_cast<int64_t>(cnt) * (feat_words(g.n_bits[c]) + F2_Y_WORDS);
+        g.row_off[c] = v;
+    }
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o);
+    if ((threadIdx.x & 63) == 0) sW[threadIdx.x >> 6] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t t = 0;
+        for (int w = 0; w < 16; ++w) t += sW[w];
+        g.blk[blockIdx.x] = t;
+    }
+}
+
+// one workgroup: exclusive scan of the blocks' words, the total last
+__global__ __launch_bounds__(1024) void k_grp_scan(GroupArgs g) {
+    __shared__ int64_t sWave[16];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int nblk = (g.num_ctx + 1023) / 1024;
+    int64_t carry = 0;
+    for (int b0 = 0; b0 < nblk; b0 += 1024) {
+        const int b = b0 + tid;
+        const int64_t v = b < nblk ? g.blk[b] : 0;
+        int64_t x = v;
+        for (int o = 1; o < 64; o <<= 1) {
+            const int64_t t = __shfl_up(x, o);
+            if (lane >= o) x += t;
+        }
+        if (lane == 63) sWave[tid >> 6] = x;
+        __syncthreads();
+        int64_t run = x - v, total = 0;
+        for (int w = 0; w < 16; ++w) {
+            total += sWave[w];
+            if (w < (tid >> 6)) run += sWave[w];
+        }
+        if (b < nblk) g.blk[b] = carry + run;
+        carry += total;
+        __syncthreads();
+    }
+    if (tid == 0) g.blk[nblk] = carry;
+}
+
+// each context's word offset: its block's offset plus the scan within the block
+__global__ __launch_bounds__(1024) void k_grp_offsets(GroupArgs g) {
+    __shared__ int64_t sWave[16];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int c = blockIdx.x * 1024 + tid;
+    const int64_t v = c < g.num_ctx ? g.row_off[c] : 0;
+    int64_t x = v;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int64_t t = __shfl_up(x, o);
+        if (lane >= o) x += t;
+    }
+    if (lane == 63) sWave[tid >> 6] = x;
+    __syncthreads();
+    int64_t run = g.blk[blockIdx.x] + x - v;
+    for (int w = 0; w < (tid >> 6); ++w) run += sWave[w];
+    if (c < g.num_ctx) g.row_off[c] = run;
+    if (c == g.num_ctx - 1) g.row_off[g.num_ctx] = g.blk[(g.num_ctx + 1023) / 1024];
+}
+
+// the dropped-row count out, and row_off[0] = 0 when there are no contexts
+__global__ __launch_bounds__(64) void k_grp_finish(GroupArgs g, int64_t* dropped_out, int no_ctx) {
+    if (threadIdx.x == 0) {
+        *dropped_out = g.nr > 0 ? *g.dropped : 0;
+        if (no_ctx) g.row_off[0] = 0;
+    }
+}
+
+// output rows: sorted position i copies its row, trimmed to the context's width
+__global__ __launch_bounds__(256) void k_grp_copy(GroupArgs g) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= g.nr) return;
+    const int2 pr = g.in[i];
+    if (pr.x >= g.num_ctx) return;
+    const int W = feat_words(g.n_bits[pr.x]) + F2_Y_WORDS;
+    const uint64_t* src = g.rows + static_cast<int64_t>(pr.y) * g.stride;
+    uint64_t* dst = g.rows_out + g.row_off[pr.x] + static_cast<int64_t>(i - g.first[pr.x]) * W;
+    for (int w = 0; w < W; ++w) dst[w] = src[w];
+}
+
 inline size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+
+// workspace of the grouping: two pair buffers, histograms, per-context bounds
+struct GroupPlan {
+    int blocks;
+    int64_t qc;
+    size_t off_a, off_b, off_hist, off_total, off_first, off_count, off_blk, off_drop, bytes;
+};
+GroupPlan group_workspace(int32_t num_ctx, int64_t nr) {
+    GroupPlan p{};
+    int64_t blocks = (nr + 8191) / 8192;
+    if (blocks > kMaxSortBlocks) blocks = kMaxSortBlocks;
+    if (blocks < 1) blocks = 1;
+    p.qc = (nr + blocks - 1) / blocks;
+    if (p.qc < 1) p.qc = 1;
+    p.blocks = static_cast<int>((nr + p.qc - 1) / p.qc);
+    if (p.blocks < 1) p.blocks = 1;
+    size_t o = 0;
+    p.off_a = o;
+    o = align256(o + sizeof(int2) * static_cast<size_t>(nr));
+    p.off_b = o;
+    o = align256(o + sizeof(int2) * static_cast<size_t>(nr));
+    p.off_hist = o;
+    o = align256(o + sizeof(int32_t) * static_cast<size_t>(p.blocks) * kGrpBins);
+    p.off_total = o;
+    o = align256(o + sizeof(int32_t) * kGrpBins);
+    p.off_first = o;
+    o = align256(o + sizeof(int32_t) * static_cast<size_t>(num_ctx));
+    p.off_count = o;
+    o = align256(o + sizeof(int32_t) * static_cast<size_t>(num_ctx));
+    p.off_blk = o;
+    o = align256(o + sizeof(int64_t) * (static_cast<size_t>((num_ctx + 1023) / 1024) + 1));
+    p.off_drop = o;
+    o = align256(o + sizeof(int64_t));
+    p.bytes = o;
+    return p;
+}
 
 // workgroups of a fit class kernel: at most one per context, at most `cap`
 unsigned fit_grid(int num_ctx, int cap) { return static_cast<unsigned>(num_ctx < cap ? num_ctx : cap); }
@@ -3381,6 +3641,81 @@ size_t f2_pool_workspace_bytes(const f2_model* members_model, int32_t num_pools)
            align256(sizeof(uint64_t) * static_cast<size_t>(members_model->basis_words)) +
            align256(sizeof(int64_t) * (static_cast<size_t>((num_pools + 255) / 256) + 1)) +
            f2_fit_workspace_bytes(num_pools);
+}
+
+size_t f2_group_workspace_bytes(int32_t num_ctx, int64_t num_rows) {
+    if (num_ctx < 0 || num_rows < 0 || num_rows > 0x7fffffff) return 0;
+    return group_workspace(num_ctx, num_rows).bytes;
+}
+
+int f2_group_rows(const int32_t* ctx_id, const uint64_t* rows, int32_t row_stride_words, int64_t num_rows,
+                  const int32_t* n_bits, int32_t num_ctx, uint64_t* rows_out, int64_t rows_out_words,
+                  int64_t* row_off_out, int64_t* dropped_out, void* workspace, size_t workspace_bytes, void* stream) {
+    if (num_ctx < 0 || num_rows < 0 || num_rows > 0x7fffffff || row_stride_words < F2_Y_WORDS + 1) return F2_EINVAL;
+    if (!row_off_out || !dropped_out || (num_ctx > 0 && !n_bits)) return F2_EINVAL;
+    if (num_rows > 0 && (!ctx_id || !rows || !rows_out || rows_out_words < num_rows * row_stride_words))
+        return F2_EINVAL;
+    if (!workspace || workspace_bytes < f2_group_workspace_bytes(num_ctx, num_rows) ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u))
+        return F2_EWORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const GroupPlan p = group_workspace(num_ctx, num_rows);
+    char* ws = static_cast<char*>(workspace);
+    GroupArgs g;
+    g.num_ctx = num_ctx;
+    g.n_bits = n_bits;
+    g.ctx_id = ctx_id;
+    g.rows = rows;
+    g.stride = row_stride_words;
+    g.nr = num_rows;
+    g.blocks = p.blocks;
+    g.qc = p.qc;
+    g.hist = reinterpret_cast<int32_t*>(ws + p.off_hist);
+    g.total = reinterpret_cast<int32_t*>(ws + p.off_total);
+    g.first = reinterpret_cast<int32_t*>(ws + p.off_first);
+    g.count = reinterpret_cast<int32_t*>(ws + p.off_count);
+    g.blk = reinterpret_cast<int64_t*>(ws + p.off_blk);
+    g.rows_out = rows_out;
+    g.row_off = row_off_out;
+    g.dropped = reinterpret_cast<int64_t*>(ws + p.off_drop);
+    int2* bufs[2] = {reinterpret_cast<int2*>(ws + p.off_a), reinterpret_cast<int2*>(ws + p.off_b)};
+    // passes: 8 bits of the key (0 .. num_ctx) each
+    int bits = 1;
+    while ((int64_t{1} << bits) <= num_ctx) ++bits;
+    const int passes = (bits + 7) / 8;
+    SortArgs cs{};
+    cs.nb = kGrpBins;
+    cs.blocks = p.blocks;
+    cs.hist = g.hist;
+    cs.total = g.total;
+    g.in = nullptr;
+    if (num_rows > 0) {
+        for (int k = 0; k < passes; ++k) {
+            g.shift = 8 * k;
+            g.out = bufs[k & 1];
+            hipLaunchKernelGGL(k_grp_count, dim3(p.blocks), dim3(kGrpThreads), 0, s, g);
+            hipLaunchKernelGGL(k_enc_colscan, dim3((kGrpBins + 63) / 64), dim3(64 * kColWaves), 0, s, cs);
+            hipLaunchKernelGGL(k_grp_scatter, dim3(p.blocks), dim3(kGrpThreads), 0, s, g);
+            g.in = g.out;
+        }
+    }
+    const unsigned cb = static_cast<unsigned>((num_ctx + 255) / 256);
+    if (num_ctx > 0) hipLaunchKernelGGL(k_grp_clear, dim3(cb), dim3(256), 0, s, g);
+    else hipLaunchKernelGGL(k_grp_clear, dim3(1), dim3(256), 0, s, g);
+    if (num_rows > 0)
+        hipLaunchKernelGGL(k_grp_bounds, dim3(static_cast<unsigned>((num_rows + 255) / 256)), dim3(256), 0, s, g);
+    const unsigned kb = static_cast<unsigned>((num_ctx + 1023) / 1024);
+    if (num_ctx > 0) {
+        hipLaunchKernelGGL(k_grp_words, dim3(kb), dim3(1024), 0, s, g);
+        hipLaunchKernelGGL(k_grp_scan, dim3(1), dim3(1024), 0, s, g);
+        hipLaunchKernelGGL(k_grp_offsets, dim3(kb), dim3(1024), 0, s, g);
+    } else {
+        hipLaunchKernelGGL(k_grp_scan, dim3(1), dim3(1024), 0, s, g);  // row_off[0] = 0 below
+    }
+    if (num_rows > 0 && num_ctx > 0)
+        hipLaunchKernelGGL(k_grp_copy, dim3(static_cast<unsigned>((num_rows + 255) / 256)), dim3(256), 0, s, g);
+    hipLaunchKernelGGL(k_grp_finish, dim3(1), dim3(64), 0, s, g, dropped_out, num_ctx == 0 ? 1 : 0);
+    return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 
 int f2_pool_bases(const f2_model* members_model, const uint64_t* out_mask, const int64_t* pool_off,

@@ -27,7 +27,7 @@ POOL_SHARED, POOL_CONTRADICTION, POOL_WIDTH_MISMATCH, POOL_MASK_MISMATCH, POOL_B
 # every entry point the header declares
 EXPORTS = ("f2_fit_layout", "f2_fit_workspace_bytes", "f2_fit_batch", "f2_encode_workspace_bytes",
            "f2_encode_batch", "f2_vectorize_rows", "f2_merge_words", "f2_pool_workspace_bytes", "f2_pool_bases",
-           "f2_status_string")
+           "f2_group_workspace_bytes", "f2_group_rows", "f2_status_string")
 
 
 class f2_model(ctypes.Structure):
@@ -76,6 +76,10 @@ def _load():
     L.f2_pool_workspace_bytes.restype = sz
     L.f2_pool_bases.argtypes = [MP, P, P, P, i64, MP, P, P, sz, P]
     L.f2_pool_bases.restype = ctypes.c_int
+    L.f2_group_workspace_bytes.argtypes = [i32, i64]
+    L.f2_group_workspace_bytes.restype = sz
+    L.f2_group_rows.argtypes = [P, P, i32, i64, P, i32, P, i64, P, P, P, sz, P]
+    L.f2_group_rows.restype = ctypes.c_int
     L.f2_status_string.argtypes = [ctypes.c_int]
     L.f2_status_string.restype = ctypes.c_char_p
     return L
@@ -206,6 +210,18 @@ def f2_pool_bases(members_model: "Model", out_mask, pool_off, members, num_membe
                                  int(workspace_bytes), _stream(stream)))
 
 
+def f2_group_workspace_bytes(num_ctx: int, num_rows: int) -> int:
+    return int(lib.f2_group_workspace_bytes(int(num_ctx), int(num_rows)))
+
+
+def f2_group_rows(ctx_id, rows, row_stride_words: int, num_rows: int, n_bits, num_ctx: int, rows_out,
+                  rows_out_words: int, row_off_out, dropped_out, workspace, workspace_bytes: int, stream=None) -> int:
+    """Enqueue the grouping of an interleaved row stream by context; returns the status code."""
+    return int(lib.f2_group_rows(_ptr(ctx_id), _ptr(rows), int(row_stride_words), int(num_rows), _ptr(n_bits),
+                                 int(num_ctx), _ptr(rows_out), int(rows_out_words), _ptr(row_off_out),
+                                 _ptr(dropped_out), _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
 # ---- convenience wrappers used by tests and the benchmark (allocation + one call) ----
 
 def workspace(nbytes: int, device="cuda"):
@@ -221,6 +237,24 @@ def fit(rows_dev, row_off_dev, n_bits_host, stream=None):
     _check(f2_fit_batch(rows_dev, rows_dev.numel(), row_off_dev, model, ws, nb, stream), "f2_fit_batch")
     model._fit_ws = ws
     return model
+
+
+def group(ctx_id_dev, rows_dev, stride: int, n_bits_dev, stream=None):
+    """Group an interleaved row stream by context; returns (rows_out, row_off, dropped) device tensors."""
+    import torch
+    dev = rows_dev.device
+    R = int(ctx_id_dev.numel())
+    C = int(n_bits_dev.numel())
+    rows_out = torch.empty(max(R * stride, 1), dtype=torch.int64, device=dev)
+    row_off = torch.empty(C + 1, dtype=torch.int64, device=dev)
+    dropped = torch.empty(1, dtype=torch.int64, device=dev)
+    nb = f2_group_workspace_bytes(C, R)
+    ws = workspace(nb, dev)
+    _check(f2_group_rows(ctx_id_dev, rows_dev, stride, R, n_bits_dev, C, rows_out, R * stride, row_off, dropped,
+                         ws, nb, stream), "f2_group_rows")
+    out_ws = ws  # kept alive with the outputs until the stream has run
+    rows_out._group_ws = out_ws
+    return rows_out, row_off, dropped
 
 
 def pool(members_model: Model, pool_off_dev, members_dev, pooled_n_host, out_mask_dev=None, stream=None):
