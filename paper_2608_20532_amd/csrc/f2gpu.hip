@@ -3053,13 +3053,14 @@ __global__ __launch_bounds__(256) void k_pool_finish(PoolArgs P) {
 // interleaved-stream ingestion: the rows of many contexts arrive mixed, in
 // stream order (Sec. 3: observations are gathered across a corpus); the fit takes
 // each context's rows contiguous and in stream order.  A stable LSD radix sort of
-// (context, row) pairs by context, 8 bits per pass (per-block LDS histograms, the
+// (context, row) pairs by context, 9 bits per pass (per-block LDS histograms, the
 // column scan of the encode sort, a stable scatter), then each context's rows are
 // copied, trimmed to its row width, to their offsets.  Rows of an out-of-range
 // context, of a width outside [0, F2_MAX_N_BITS], or wider than the stride sort
 // last and are dropped.
 // ---------------------------------------------------------------------------
-constexpr int kGrpBins = 256;
+constexpr int kGrpDigitBits = 9;  // two passes up to 2^18 - 1 contexts
+constexpr int kGrpBins = 1 << kGrpDigitBits;
 constexpr int kGrpThreads = 1024;
 constexpr int kGrpWaves = kGrpThreads / 64;
 
@@ -3072,7 +3073,7 @@ struct GroupArgs {
     int64_t nr;             // rows
     int32_t blocks;
     int64_t qc;             // rows per count / scatter block
-    int32_t shift;          // digit of this pass: (key >> shift) & 255
+    int32_t shift;          // digit of this pass: (key >> shift) & (kGrpBins - 1)
     const int2* in;         // pairs (key, row) of the previous pass, or null (first pass: from ctx_id)
     int2* out;
     int32_t* hist;          // [blocks][kGrpBins]
@@ -3136,7 +3137,7 @@ __global__ __launch_bounds__(kGrpThreads) void k_grp_scatter(GroupArgs g) {
         const int dg = (pr.x >> g.shift) & (kGrpBins - 1);
         uint64_t peers = __ballot(live);
 #pragma unroll
-        for (int b = 0; b < 8; ++b) {
+        for (int b = 0; b < kGrpDigitBits; ++b) {
             const uint64_t m = __ballot(live && ((dg >> b) & 1));
             peers &= ((dg >> b) & 1) ? m : ~m;
         }
@@ -3260,15 +3261,22 @@ __global__ __launch_bounds__(64) void k_grp_finish(GroupArgs g, int64_t* dropped
 }
 
 // output rows: sorted position i copies its row, trimmed to the context's width
+// eight lanes per row: lane j copies words j, j + 8, ... of its row, so one
+// instruction moves up to 64 contiguous bytes of each of 8 rows and no lane waits on
+// a chain of single-word copies
+constexpr int kGrpCopyLanes = 8;
+constexpr int kGrpCopyRowsPerBlock = 256 / kGrpCopyLanes;
 __global__ __launch_bounds__(256) void k_grp_copy(GroupArgs g) {
-    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (i >= g.nr) return;
-    const int2 pr = g.in[i];
-    if (pr.x >= g.num_ctx) return;
-    const int W = feat_words(g.n_bits[pr.x]) + F2_Y_WORDS;
-    const uint64_t* src = g.rows + static_cast<int64_t>(pr.y) * g.stride;
-    uint64_t* dst = g.rows_out + g.row_off[pr.x] + static_cast<int64_t>(i - g.first[pr.x]) * W;
-    for (int w = 0; w < W; ++w) dst[w] = src[w];
+    const int j = threadIdx.x % kGrpCopyLanes;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kGrpCopyRowsPerBlock + threadIdx.x / kGrpCopyLanes;
+         i < g.nr; i += static_cast<int64_t>(gridDim.x) * kGrpCopyRowsPerBlock) {
+        const int2 pr = g.in[i];
+        if (pr.x >= g.num_ctx) continue;
+        const int W = feat_words(g.n_bits[pr.x]) + F2_Y_WORDS;
+        const uint64_t* __restrict__ src = g.rows + static_cast<int64_t>(pr.y) * g.stride;
+        uint64_t* __restrict__ dst = g.rows_out + g.row_off[pr.x] + static_cast<int64_t>(i - g.first[pr.x]) * W;
+        for (int w = j; w < W; w += kGrpCopyLanes) dst[w] = src[w];
+    }
 }
 
 inline size_t align256(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
@@ -3679,10 +3687,10 @@ int f2_group_rows(const int32_t* ctx_id, const uint64_t* rows, int32_t row_strid
     g.row_off = row_off_out;
     g.dropped = reinterpret_cast<int64_t*>(ws + p.off_drop);
     int2* bufs[2] = {reinterpret_cast<int2*>(ws + p.off_a), reinterpret_cast<int2*>(ws + p.off_b)};
-    // passes: 8 bits of the key (0 .. num_ctx) each
+    // passes: kGrpDigitBits bits of the key (0 .. num_ctx) each
     int bits = 1;
     while ((int64_t{1} << bits) <= num_ctx) ++bits;
-    const int passes = (bits + 7) / 8;
+    const int passes = (bits + kGrpDigitBits - 1) / kGrpDigitBits;
     SortArgs cs{};
     cs.nb = kGrpBins;
     cs.blocks = p.blocks;
@@ -3691,7 +3699,7 @@ int f2_group_rows(const int32_t* ctx_id, const uint64_t* rows, int32_t row_strid
     g.in = nullptr;
     if (num_rows > 0) {
         for (int k = 0; k < passes; ++k) {
-            g.shift = 8 * k;
+            g.shift = kGrpDigitBits * k;
             g.out = bufs[k & 1];
             hipLaunchKernelGGL(k_grp_count, dim3(p.blocks), dim3(kGrpThreads), 0, s, g);
             hipLaunchKernelGGL(k_enc_colscan, dim3((kGrpBins + 63) / 64), dim3(64 * kColWaves), 0, s, cs);
@@ -3713,7 +3721,9 @@ int f2_group_rows(const int32_t* ctx_id, const uint64_t* rows, int32_t row_strid
         hipLaunchKernelGGL(k_grp_scan, dim3(1), dim3(1024), 0, s, g);  // row_off[0] = 0 below
     }
     if (num_rows > 0 && num_ctx > 0)
-        hipLaunchKernelGGL(k_grp_copy, dim3(static_cast<unsigned>((num_rows + 255) / 256)), dim3(256), 0, s, g);
+        hipLaunchKernelGGL(k_grp_copy,
+                           dim3(static_cast<unsigned>(std::min<int64_t>((num_rows + kGrpCopyRowsPerBlock - 1) / kGrpCopyRowsPerBlock, 1 << 20))),
+                           dim3(256), 0, s, g);
     hipLaunchKernelGGL(k_grp_finish, dim3(1), dim3(64), 0, s, g, dropped_out, num_ctx == 0 ? 1 : 0);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }

@@ -26,11 +26,12 @@ def _run(f2, ids, rows, stride, n_bits):
     return parity.host(out, np.uint64)[:int(off_h[-1])], off_h, int(parity.host(dropped, np.int64)[0])
 
 
-@pytest.mark.parametrize("C,R,S", [(300, 200_000, 6), (3, 1000, 4), (70_000, 150_000, 7)])
+@pytest.mark.parametrize("C,R,S", [(300, 200_000, 6), (3, 1000, 4), (70_000, 150_000, 7), (300_000, 400_000, 5)])
 def test_group_random_stream(f2, C, R, S):
     """Random ids (some out of range), widths up to 300 (some rows wider than the
     stride, one width outside the supported range): rows, offsets and the dropped
-    count equal the oracle's; 70,000 contexts take three radix passes."""
+    count equal the oracle's; 300 contexts take one radix pass, 70,000 two and
+    300,000 three."""
     rng = np.random.default_rng(C)
     n_bits = rng.integers(0, 300, size=C).astype(np.int32)
     n_bits[0] = 4096 if C > 1 else n_bits[0]
