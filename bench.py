@@ -4,18 +4,23 @@
 A step is one pass of the whole path over one batch of synthetic input that is
 already resident in HBM: f2_fit_batch over every context (plan, reduce,
 classify, insert, finalize) followed by f2_encode_batch over the query batch
-against the model just fitted.  Default workload: 4,096 contexts of widths
-17..97 (16..96 uniform input bits plus one reserved bit), 2(n+1) rows each
-(468,656 rows, 13.5 MB), 5% contradictory, then 1M queries (stride 2 words)
-with 2% outside the span.
+against the model just fitted.  Default workload ("step"): the 80,000-context
+fit (widths 8..256, lognormal row counts, 7.24M rows, 1% contradictory), then
+100M Zipf(1.1) queries (stride 4 words, 1% outside the span) encoded against the
+80,000 maps just fitted.  The other configurations (the 64 wide contexts of
+width 4,095, the 4,096-context batch with 1M queries, the single context) are
+timed the same way and reported under "other_configs" of the same line.
 
 Prints one JSON line.  `value` is fit rows/s over the fit phase of the timed
 steps; encode words/s and per-phase figures are reported beside it.  Each phase
 is one library call, timed with HIP events on the stream it is enqueued on.
 The roofline object describes the phase that takes longer: its algorithmic HBM
-bytes per call over its average duration, against the 8 TB/s HBM peak, and the
-measured HBM traffic of its kernels from the committed rocprofv3 counter
-summary when that summary was taken on the current kernel source.
+bytes per call over its average duration, against the 8 TB/s HBM peak (the
+wide-context fit: algorithmic 32-bit operations against the integer issue
+peak), with the rate a streaming copy or an XOR issue probe reaches on the same
+GPU beside it, and the measured HBM traffic of its kernels from the committed
+rocprofv3 counter summary when that summary was taken on the current kernel
+source.
 """
 import argparse
 import hashlib
@@ -35,6 +40,10 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
 
 WORKLOADS = {
     # name: (fit recipe, contexts, queries, stride, out-of-span fraction, zipf exponent, description)
+    "step": (3, 80000, 100_000_000, 4, 0.01, 1.1,
+             "fit 80000 contexts, n in [8,256] geometric (mean 40), lognormal rows (median 30, max 4000), "
+             "x in a random 0.7n-dim subspace, 1% contradictory (7.24M rows); then encode 100M Zipf(1.1) "
+             "queries, stride 4, 1% out of span, against the 80000 maps just fitted"),
     "recipe2": (2, 4096, 1_000_000, 2, 0.02, 0.0,
                 "fit 4096 contexts, n in [17,97] (16-96 uniform bits + 1 reserved), 2(n+1) rows, 5% contradictory; "
                 "encode 1M uniform queries, stride 2, 2% out of span"),
@@ -403,13 +412,175 @@ def bench_group(args):
     }), flush=True)
 
 
+def host_cpu():
+    """CPU model and core counts of the host the oracle baseline runs on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"cpu_model": model, "nproc": usable, "cpu_count": os.cpu_count()}
+
+
+def measured_ceilings(stream):
+    """Achievable rates from the probe library: a streaming copy (GB/s, bytes read plus
+    written) and a run of independent 32-bit bitwise VALU instructions (T lane ops/s)."""
+    import numpy as np
+    import torch
+    from paper_2608_20532_amd import f2probe
+    dev = torch.device("cuda:0")
+    words = (1 << 30) // 8  # 1 GiB each way
+    src = torch.ones(words, dtype=torch.int64, device=dev)
+    dst = torch.empty_like(src)
+    out = torch.empty(256 * 256 * 8, dtype=torch.int32, device=dev)
+    sp = stream.cuda_stream
+
+    def timed(call, reps):
+        for _ in range(2):
+            assert call() == 0
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ms = []
+        for _ in range(reps):
+            ev[0].record(stream)
+            assert call() == 0
+            ev[1].record(stream)
+            torch.cuda.synchronize()
+            ms.append(ev[0].elapsed_time(ev[1]))
+        return float(np.median(ms))
+
+    copy_ms = timed(lambda: f2probe.f2probe_copy(src, dst, words, sp), 10)
+    assert bool(torch.equal(src[:1024], dst[:1024]))
+    blocks, iters = 256 * 8 * 4, 4096
+    res = {"copy_GBps": 2 * 8 * words / (copy_ms * 1e-3) / 1e9, "copy_bytes": 2 * 8 * words}
+    for op, name in ((0, "xor_Tops"), (1, "bitop3_Tops")):
+        ms = timed(lambda: f2probe.f2probe_bitops(out, blocks, iters, op, sp), 5)
+        res[name] = blocks * 256 * iters * 16 / (ms * 1e-3) / 1e12
+    del src, dst, out
+    torch.cuda.empty_cache()
+    return res
+
+
+def time_fit_encode(f2gpu, wl, ctx, x, stride, nq, do_fit, steps, warmup, stream):
+    """Upload a workload, then W untimed and K timed steps (fit then encode); returns the
+    per-phase averages of HIP events recorded on the stream the library enqueues on."""
+    import numpy as np
+    import torch
+    dev = torch.device("cuda:0")
+    to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int64) if a.dtype == np.uint64 else a).to(dev)
+    rows_d, off_d = to_dev(wl.rows), to_dev(wl.row_off)
+    model = f2gpu.Model(wl.n_bits, device=dev)
+    fws = f2gpu.f2_fit_workspace_bytes(model.num_ctx)
+    fit_ws = f2gpu.workspace(fws, dev)
+    if nq:
+        ctx_d, x_d = to_dev(ctx), to_dev(x)
+        words = torch.empty((nq, 2), dtype=torch.int64, device=dev)
+        qf = torch.empty(nq, dtype=torch.uint8, device=dev)
+        ews = f2gpu.f2_encode_workspace_bytes(model, nq)
+        enc_ws = f2gpu.workspace(ews, dev)
+    sptr = stream.cuda_stream
+
+    def check(st, what):
+        if st != 0:
+            raise RuntimeError(f"{what}: {f2gpu.f2_status_string(st)}")
+
+    def fit():
+        check(f2gpu.f2_fit_batch(rows_d, wl.rows.size, off_d, model, fit_ws, fws, sptr), "fit")
+
+    def encode():
+        check(f2gpu.f2_encode_batch(model, ctx_d, x_d, stride, nq, words, qf, enc_ws, ews, sptr), "encode")
+
+    if not do_fit:
+        fit()
+    for _ in range(warmup):
+        if do_fit:
+            fit()
+        if nq:
+            encode()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for k in range(steps):
+        ev[k][0].record(stream)
+        if do_fit:
+            fit()
+        ev[k][1].record(stream)
+        if nq:
+            encode()
+        ev[k][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    fit_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) if do_fit else 0.0
+    enc_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) if nq else 0.0
+    rank = model.rank.cpu().numpy()[:wl.num_ctx]
+    del rows_d, off_d, model, fit_ws
+    if nq:
+        del ctx_d, x_d, words, qf, enc_ws
+    torch.cuda.empty_cache()
+    return fit_ms, enc_ms, 1e3 * wall / steps, rank
+
+
+def phases_and_roofline(name, wl, nq, stride, do_fit, fit_ms, enc_ms, rank, ceil):
+    """Per-phase algorithmic rates and the roofline object of the phase (library call) that
+    takes longer: wide-context fits against the integer issue rate, the rest against HBM."""
+    phases = {}
+    if do_fit:
+        fb = fit_bytes(wl, rank)
+        phases["fit"] = {"call": "f2_fit_batch", "ms": fit_ms, "bytes": fb, "GBps": fb / (fit_ms * 1e-3) / 1e9}
+    if nq:
+        eb = encode_bytes(wl, nq, stride)
+        phases["encode"] = {"call": "f2_encode_batch", "ms": enc_ms, "bytes": eb,
+                            "GBps": eb / (enc_ms * 1e-3) / 1e9}
+    dom = max(phases, key=lambda k: phases[k]["ms"])
+    traffic, why = load_traffic(name)
+    tr = traffic.get(dom) if traffic else None
+    if name == "recipe4":
+        # wide contexts: the blocked elimination is bound by integer VALU work, not by HBM
+        ops = fit_int_ops(wl, rank)
+        tops = ops / (fit_ms * 1e-3) / 1e12
+        phases["fit"]["int_ops"] = ops
+        roof = {"bound": "alu", "kernel": phases[dom]["call"], "achieved": tops, "peak": INT_PEAK_TOPS,
+                "unit": "Tops/s (32-bit integer lane ops)", "frac": tops / INT_PEAK_TOPS,
+                "traffic": tr["bytes"] if tr else None, "algorithmic_ops": ops,
+                "algorithmic_bytes": phases[dom]["bytes"], "avg_ms": phases[dom]["ms"]}
+        if ceil:
+            roof["measured_peak"] = ceil["xor_Tops"]
+            roof["measured_peak_unit"] = "Tops/s, v_xor_b32 issue (probe)"
+            roof["frac_of_measured_peak"] = tops / ceil["xor_Tops"]
+    else:
+        roof = {"bound": "hbm", "kernel": phases[dom]["call"], "achieved": phases[dom]["GBps"], "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": phases[dom]["GBps"] / HBM_PEAK_GBS,
+                "traffic": tr["bytes"] if tr else None,
+                "algorithmic_bytes": phases[dom]["bytes"], "avg_ms": phases[dom]["ms"]}
+        if ceil:
+            roof["measured_peak"] = ceil["copy_GBps"]
+            roof["measured_peak_unit"] = "GB/s, streaming copy (probe)"
+            roof["frac_of_measured_peak"] = phases[dom]["GBps"] / ceil["copy_GBps"]
+    if tr:
+        roof["kernels"] = tr["kernels"]
+    else:
+        roof["traffic_note"] = why or f"no counters for the {dom} phase of this workload"
+    return phases, roof
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="recipe2", choices=sorted(WORKLOADS) + sorted(STREAM_WORKLOADS))
+    ap.add_argument("--workload", default="step", choices=sorted(WORKLOADS) + sorted(STREAM_WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="default step only: skip the other configurations reported beside it")
+    ap.add_argument("--no-ceilings", action="store_true", help="skip the copy and integer-issue probes")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -448,7 +619,7 @@ def main():
 
     recipe, num_ctx, nq, stride, frac, zipf, desc = WORKLOADS[args.workload]
     torch.cuda.set_device(0)
-    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()  # the library enqueues every kernel on this stream
     t0 = time.time()
     wl = synth.fit_workload(recipe, num_ctx=num_ctx)
     ctx = x = None
@@ -456,93 +627,39 @@ def main():
         ctx, x, _ = synth.queries(wl, nq, stride, frac, zipf)
     print(f"[bench] generated {args.workload}: {wl.num_ctx} contexts, {wl.total_rows} rows, {nq} queries "
           f"in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
-
-    to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int64) if a.dtype == np.uint64 else a).to(dev)
-    rows_d, off_d = to_dev(wl.rows), to_dev(wl.row_off)
-    model = f2gpu.Model(wl.n_bits, device=dev)
-    fws = f2gpu.f2_fit_workspace_bytes(model.num_ctx)
-    fit_ws = f2gpu.workspace(fws, dev)
-    if nq:
-        ctx_d, x_d = to_dev(ctx), to_dev(x)
-        words = torch.empty((nq, 2), dtype=torch.int64, device=dev)
-        qf = torch.empty(nq, dtype=torch.uint8, device=dev)
-        ews = f2gpu.f2_encode_workspace_bytes(model, nq)
-        enc_ws = f2gpu.workspace(ews, dev)
-    stream = torch.cuda.current_stream()  # the library enqueues every kernel on this stream
-    sptr = stream.cuda_stream
     do_fit = args.workload != "recipe5"
-
-    def check(st, what):
-        if st != 0:
-            raise RuntimeError(f"{what}: {f2gpu.f2_status_string(st)}")
-
-    def fit():
-        check(f2gpu.f2_fit_batch(rows_d, wl.rows.size, off_d, model, fit_ws, fws, sptr), "fit")
-
-    def encode():
-        check(f2gpu.f2_encode_batch(model, ctx_d, x_d, stride, nq, words, qf, enc_ws, ews, sptr), "encode")
-
-    if not do_fit:
-        fit()
-    for _ in range(args.warmup):
-        if do_fit:
-            fit()
-        if nq:
-            encode()
-    torch.cuda.synchronize()
-    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
-
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    for k in range(args.steps):
-        ev[k][0].record(stream)
-        if do_fit:
-            fit()
-        ev[k][1].record(stream)
-        if nq:
-            encode()
-        ev[k][2].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    fit_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev])) if do_fit else 0.0
-    enc_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev])) if nq else 0.0
-    step_ms = 1e3 * wall / args.steps
+    fit_ms, enc_ms, step_ms, rank = time_fit_encode(f2gpu, wl, ctx, x, stride, nq, do_fit, args.steps, args.warmup,
+                                                    stream)
     print(f"[bench] timed {args.steps} steps: fit {fit_ms:.4f} ms, encode {enc_ms:.4f} ms, wall/step {step_ms:.4f} ms",
           file=sys.stderr, flush=True)
+    ceil = None
+    if not args.no_ceilings:
+        ceil = measured_ceilings(stream)
+        print(f"[bench] ceilings: copy {ceil['copy_GBps']:.0f} GB/s, xor {ceil['xor_Tops']:.1f} T/s, "
+              f"bitop3 {ceil['bitop3_Tops']:.1f} T/s", file=sys.stderr, flush=True)
+    phases, roof = phases_and_roofline(args.workload, wl, nq, stride, do_fit, fit_ms, enc_ms, rank, ceil)
 
-    rank = model.rank.cpu().numpy()[:wl.num_ctx]
-    phases = {}
-    if do_fit:
-        fb = fit_bytes(wl, rank)
-        phases["fit"] = {"call": "f2_fit_batch", "ms": fit_ms, "bytes": fb, "GBps": fb / (fit_ms * 1e-3) / 1e9}
-    if nq:
-        eb = encode_bytes(wl, nq, stride)
-        phases["encode"] = {"call": "f2_encode_batch", "ms": enc_ms, "bytes": eb,
-                            "GBps": eb / (enc_ms * 1e-3) / 1e9}
-    dom = max(phases, key=lambda k: phases[k]["ms"])
-    traffic, why = load_traffic(args.workload)
-    tr = traffic.get(dom) if traffic else None
-    if args.workload == "recipe4":
-        # wide contexts: the blocked elimination is bound by integer VALU work, not by HBM
-        ops = fit_int_ops(wl, rank)
-        tops = ops / (fit_ms * 1e-3) / 1e12
-        phases["fit"]["int_ops"] = ops
-        roof = {"bound": "alu", "kernel": phases[dom]["call"], "achieved": tops, "peak": INT_PEAK_TOPS,
-                "unit": "Tops/s (32-bit integer lane ops)", "frac": tops / INT_PEAK_TOPS,
-                "traffic": tr["bytes"] if tr else None, "algorithmic_ops": ops,
-                "algorithmic_bytes": phases[dom]["bytes"], "avg_ms": phases[dom]["ms"]}
-    else:
-        roof = {"bound": "hbm", "kernel": phases[dom]["call"], "achieved": phases[dom]["GBps"], "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": phases[dom]["GBps"] / HBM_PEAK_GBS,
-                "traffic": tr["bytes"] if tr else None,
-                "algorithmic_bytes": phases[dom]["bytes"], "avg_ms": phases[dom]["ms"]}
-    if tr:
-        roof["kernels"] = tr["kernels"]
-    else:
-        roof["traffic_note"] = why or f"no counters for the {dom} phase of this workload"
+    extras = {}
+    if args.workload == "step" and not args.no_extras:
+        # the other configurations, timed the same way (no oracle baseline): the wide-context
+        # fit against the integer issue rate, the small ones against HBM
+        for name in ("recipe4", "recipe2", "recipe1"):
+            r2, c2, nq2, s2, f2_, z2, d2 = WORKLOADS[name]
+            wl2 = synth.fit_workload(r2, num_ctx=c2)
+            cx2 = xx2 = None
+            if nq2:
+                cx2, xx2, _ = synth.queries(wl2, nq2, s2, f2_, z2)
+            fm, em, sm, rk = time_fit_encode(f2gpu, wl2, cx2, xx2, s2, nq2, True, args.steps, args.warmup, stream)
+            ph2, rf2 = phases_and_roofline(name, wl2, nq2, s2, True, fm, em, rk, ceil)
+            extras[name] = {"workload": d2, "fit_rows_per_s": wl2.total_rows / (fm * 1e-3),
+                            "encode_words_per_s": nq2 / (em * 1e-3) if nq2 else None, "ms_per_step": sm,
+                            "phases": ph2, "roofline": rf2}
+            print(f"[bench] {name}: fit {fm:.4f} ms, encode {em:.4f} ms", file=sys.stderr, flush=True)
 
-    cpu = None if args.no_cpu_baseline else cpu_baseline(wl, ctx, x, stride, nq, do_fit)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, ctx, x, stride, nq, do_fit)
+        cpu.update(host_cpu())
     rows_per_s = wl.total_rows / (fit_ms * 1e-3) if do_fit else None
     words_per_s = nq / (enc_ms * 1e-3) if nq else None
     out = {
@@ -564,8 +681,11 @@ def main():
         "encode_words_per_s": words_per_s,
         "phases": phases,
         "roofline": roof,
+        "measured_ceilings": ceil,
         "cpu_baseline": cpu,
     }
+    if extras:
+        out["other_configs"] = extras
     print(json.dumps(out), flush=True)
 
 

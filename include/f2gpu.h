@@ -65,14 +65,21 @@ enum {
     F2_CTX_CONTRADICTION = 1u, /* n_contra > 0: some row had a zero-feature, nonzero-output residual */
     F2_CTX_BAD_SEGMENT = 2u,   /* row segment negative, past rows_words, or not a multiple of fw+2 words */
     F2_CTX_BAD_WIDTH = 4u,     /* n_bits outside [0, F2_MAX_N_BITS], or above a declared max_n_bits */
-    F2_CTX_BAD_OUTPUT = 8u     /* output offsets of this context fall outside the output buffers */
+    F2_CTX_BAD_OUTPUT = 8u,    /* output offsets of this context fall outside the output buffers */
+    F2_CTX_SYNC_TIMEOUT = 16u  /* a wide context fitted by several workgroups together: a bounded wait
+                                  for the other workgroups gave up, so the outputs of this context
+                                  are not trustworthy; encoding treats it like a malformed context.
+                                  The wait bound is 2^24 polls; the environment variable
+                                  F2GPU_GROUP_SPIN_LIMIT (read at every f2_fit_batch call) overrides
+                                  it, 0 meaning "never wait" (a test hook for this report) */
 };
 
 /* per-query flags (qflags_out) */
 enum {
     F2_Q_OUT_OF_SPAN = 1u,       /* phi(x) is not in the observed span: word is 0 */
     F2_Q_CTX_CONTRADICTORY = 2u, /* the context's training data held a contradiction */
-    F2_Q_BAD_CTX = 4u            /* context id out of range or context not fitted: word is 0 */
+    F2_Q_BAD_CTX = 4u            /* context id out of range, or context malformed or flagged
+                                    F2_CTX_SYNC_TIMEOUT: word is 0 */
 };
 
 /*
@@ -222,8 +229,9 @@ enum {
 /*
  * Pooling of separately fitted contexts (Sec. 2.1: groups with the same
  * instruction form are trained apart, then their bases are combined and
- * eliminated; one shared map is kept when the equations are consistent and the
- * output masks match, otherwise the maps stay separate; Sec. 2.2 merges shard
+ * eliminated; a single map serves the whole group when the combined system has
+ * no contradiction and every member learned the same output bits, else each
+ * member keeps its own; Sec. 2.2 merges shard
  * bases the same way).  Pool p has the member contexts
  * members[pool_off[p] .. pool_off[p+1]) of members_model; their basis rows, in
  * member order and each member's stored order, are fitted as one row stream

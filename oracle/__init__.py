@@ -18,7 +18,8 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SO = os.path.join(_HERE, "liboracle.so")
+# F2ORACLE_LIB may name another build of f2_oracle.c (the sanitizer build of the CPU tests)
+_SO = os.environ.get("F2ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "f2_oracle.c")
 _lib = None
 

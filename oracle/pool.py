@@ -2,9 +2,10 @@
 
 The paper trains every exact (f, m, s) group on its own, then tests whether
 groups with the same (f, m) can share one map: their bases are combined and
-eliminated; when the combined equations are consistent and the output masks
-match, one shared map is kept, otherwise the maps stay separate (Sec. 2.1, the
-paragraph after Eq. 1; the same elimination merges shard bases, Sec. 2.2).
+eliminated; a single map serves them all when the combined system has no
+contradiction and every member learned the same output bits, else each keeps
+its own (Sec. 2.1, the paragraph after Eq. 1; the same elimination merges
+shard bases, Sec. 2.2).
 
 pool_bases follows that description: for each pool, the basis rows of its
 members (in member order, each member's rows in its stored order) form one

@@ -29,6 +29,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <stdlib.h>
+
 #include <atomic>
 
 #include "../../include/f2gpu.h"
@@ -60,6 +62,7 @@ struct FitArgs {
     int32_t* plan;  // workspace: class list offsets, group barrier counters, context lists (k_fit_plan)
     int32_t coop;   // the wide kernel runs as a cooperative launch (all workgroups resident)
     int32_t max_n;  // host hint: largest width of the batch, -1 if unknown
+    int32_t spin_limit;  // polls of a group barrier before it gives up (0: never wait)
 };
 
 struct EncArgs {
@@ -83,7 +86,7 @@ struct EncArgs {
     uint8_t* qflags;
 };
 
-constexpr uint32_t kBadCtx = F2_CTX_BAD_SEGMENT | F2_CTX_BAD_WIDTH | F2_CTX_BAD_OUTPUT;
+constexpr uint32_t kBadCtx = F2_CTX_BAD_SEGMENT | F2_CTX_BAD_WIDTH | F2_CTX_BAD_OUTPUT | F2_CTX_SYNC_TIMEOUT;
 
 __device__ __forceinline__ int feat_words(int n) { return (n + 64) >> 6; }
 
@@ -258,8 +261,11 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_count(FitArgs a) {
         if (ds.bad) {
             write_bad_context(a, ds);
         } else {
-            k = fit_class(ds) * kBuckets + (kBuckets - 1 - cost_bucket(ds));
+            const int cls = fit_class(ds);
+            k = cls * kBuckets + (kBuckets - 1 - cost_bucket(ds));
             atomicAdd(&sBin[k], 1);
+            // the workgroups of a wide context OR their flags in (contradiction, wait timeout)
+            if (cls == kClsLarge) a.ctx_flags[c] = 0u;
         }
         P.key[c] = k;
     }
@@ -1135,6 +1141,7 @@ struct LargeShared {
     uint64_t pm[64];              // pivot columns of the retained basis
     uint64_t npm[64];             // pivot columns found in the current block
     int contra, nnew;
+    int timeout;                  // a group barrier of this context gave up
     long long firstMin;
 };
 
@@ -1165,11 +1172,15 @@ __device__ __forceinline__ int next_round(const LargeShared& L, int fw, int r, i
 
 // barrier of the G workgroups that fit one context together (all resident: the
 // launch is cooperative); counter `bar` only grows, epoch counts this member's
-// arrivals.  The wait is bounded so that a kernel can never hang on it.
+// arrivals.  The wait is bounded (spin_limit polls) so that a kernel can never
+// hang on it; a wait that gives up sets *timed_out (LDS, read after the
+// workgroup barrier that ends this call), and the context is reported
+// F2_CTX_SYNC_TIMEOUT.  spin_limit 0 never waits: every call gives up.
 // full: release and acquire fences around it (every earlier global write of the
 // group visible after it); otherwise only the arrival order: the data exchanged
 // across it must be written and read with device-scope atomic stores and loads.
-__device__ __forceinline__ void group_barrier(int* bar, int& epoch, int G, bool full = true) {
+__device__ __forceinline__ void group_barrier(int* bar, int& epoch, int G, int spin_limit, int* timed_out,
+                                              bool full = true) {
     if (full) __threadfence();
     __builtin_amdgcn_s_waitcnt(0);  // this thread's stores performed before the arrival is counted
     __syncthreads();
@@ -1177,10 +1188,15 @@ __device__ __forceinline__ void group_barrier(int* bar, int& epoch, int G, bool 
     if (threadIdx.x == 0) {
         __hip_atomic_fetch_add(bar, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const int target = G * epoch;
-        for (int spin = 0; spin < (1 << 24); ++spin) {
-            if (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) break;
+        bool arrived = false;
+        for (int spin = 0; spin < spin_limit; ++spin) {
+            if (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) {
+                arrived = true;
+                break;
+            }
             __builtin_amdgcn_s_sleep(2);
         }
+        if (!arrived) *timed_out = 1;
         if (full) __threadfence();
     }
     __syncthreads();
@@ -1323,6 +1339,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
     if (tid < 64) L.pm[tid] = 0;
     if (tid == 0) {
         L.contra = 0;
+        L.timeout = 0;
         L.firstMin = kNone;
     }
     int rank = 0;
@@ -1385,7 +1402,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
                 for (int k = 0; k < kLgSlots; ++k)
                     if (act) put_dev(mine + (kLgSlots * wave + k) * W + lane, acc[k]);
                 if (lane < 2 * kLgSlots) put_dev(mine + yi * W + fw + (lane & 1), yv);
-                group_barrier(bar, epoch, G, false);
+                group_barrier(bar, epoch, G, a.spin_limit, &L.timeout, false);
                 // reads past a partial's rows land in another partial or past the
                 // resource (zero); their values are masked off
                 const __amdgpu_buffer_rsrc_t xr = dev_rsrc(X + (blk & 1) * G * xs, static_cast<uint32_t>(8 * G * xs));
@@ -1636,7 +1653,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
         rank += K;
     }
 
-    if (G > 1) group_barrier(bar, epoch, G);  // every member's basis rows written
+    if (G > 1) group_barrier(bar, epoch, G, a.spin_limit, &L.timeout);  // every member's basis rows written
     if (b0 < m) {
         // full rank: every remaining row lies in the span; its residual is y + M phi
         // (members of a group take every G-th 512-row chunk)
@@ -1694,7 +1711,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
                 X[2 * g] = sCnt;
                 X[2 * g + 1] = sFirst;
             }
-            group_barrier(bar, epoch, G);
+            group_barrier(bar, epoch, G, a.spin_limit, &L.timeout);
             if (g == 0 && tid == 0) {
                 for (int o = 1; o < G; ++o) {
                     L.contra += static_cast<int>(X[2 * o]);
@@ -1706,7 +1723,18 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
             __syncthreads();
         }
     }
-    if (g != 0) return;  // member 0 writes the outputs
+    // the rank as the pivot set holds it: equal to the running count unless a
+    // timed-out exchange left members with different data, and then it keeps
+    // every output position below d
+    if (tid == 0) L.nnew = 0;
+    __syncthreads();
+    if (wave == 0 && lane < fw) atomicAdd(&L.nnew, __popcll(L.pm[lane] & lmask));
+    __syncthreads();
+    rank = L.nnew;
+    if (g != 0) {  // member 0 writes the outputs; the others only report a wait that gave up
+        if (tid == 0 && L.timeout) atomicOr(&a.ctx_flags[c], F2_CTX_SYNC_TIMEOUT);
+        return;
+    }
 
     // outputs: canonical map and encode table from the slots, then compaction into descending priority
     const int64_t po = a.piv_off[c], mo = a.map_off[c];
@@ -1802,7 +1830,8 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
         a.rank[c] = rank;
         a.n_contra[c] = L.contra;
         a.first_contra[c] = L.firstMin == kNone ? -1 : L.firstMin;
-        a.ctx_flags[c] = L.contra ? F2_CTX_CONTRADICTION : 0u;
+        // OR: the other members may report a timeout (the plan cleared the word)
+        atomicOr(&a.ctx_flags[c], (L.contra ? F2_CTX_CONTRADICTION : 0u) | (L.timeout ? F2_CTX_SYNC_TIMEOUT : 0u));
     }
     __syncthreads();
 }
@@ -3399,6 +3428,17 @@ bool model_complete(const f2_model* m) {
            m->piv_entries >= 0 && m->map_words >= 0;
 }
 
+// polls of a group barrier before it gives up: 2^24 (seconds), or the value of
+// F2GPU_GROUP_SPIN_LIMIT (a test hook for the timeout report)
+int group_spin_limit() {
+    const char* v = getenv("F2GPU_GROUP_SPIN_LIMIT");
+    if (!v || !*v) return 1 << 24;
+    char* end = nullptr;
+    const long x = strtol(v, &end, 10);
+    if (*end != '\0' || x < 0) return 1 << 24;
+    return x > (1 << 24) ? (1 << 24) : static_cast<int>(x);
+}
+
 FitArgs fit_args(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m, int32_t* plan) {
     FitArgs a;
     a.rows = rows;
@@ -3423,6 +3463,7 @@ FitArgs fit_args(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
     a.plan = plan;
     a.coop = 0;
     a.max_n = m->max_n_bits;
+    a.spin_limit = group_spin_limit();
     return a;
 }
 

@@ -1,0 +1,80 @@
+// f2probe.hip -- ceiling probes for the roofline figures (gfx950): a streaming
+// copy (achievable HBM bandwidth) and a run of independent 32-bit bitwise VALU
+// instructions (achievable integer issue rate).  Nothing here is part of the
+// fit or the encode.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/f2probe.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ __launch_bounds__(kThreads) void k_probe_copy(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                                         int64_t n16) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
+    int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    // four independent 16-byte loads in flight per thread, then their stores
+    for (; i + 3 * stride < n16; i += 4 * stride) {
+        const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+        dst[i] = a;
+        dst[i + stride] = b;
+        dst[i + 2 * stride] = c;
+        dst[i + 3 * stride] = d;
+    }
+    for (; i < n16; i += stride) dst[i] = src[i];
+}
+
+constexpr int kVals = 16;
+
+template <int OP>
+__global__ __launch_bounds__(kThreads) void k_probe_bitops(uint32_t* out, int iters) {
+    const uint32_t t = blockIdx.x * kThreads + threadIdx.x;
+    uint32_t v[kVals];
+#pragma unroll
+    for (int k = 0; k < kVals; ++k) v[k] = t * 0x9e3779b9u + static_cast<uint32_t>(k) * 0x85ebca6bu;
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int k = 0; k < kVals; ++k) {
+            if constexpr (OP == 0)
+                v[k] ^= v[(k + 1) & (kVals - 1)];
+            else
+                v[k] = __builtin_amdgcn_bitop3_b32(v[k], v[(k + 1) & (kVals - 1)], v[(k + 5) & (kVals - 1)], 0x96);
+        }
+    }
+    uint32_t r = 0;
+#pragma unroll
+    for (int k = 0; k < kVals; ++k) r += v[k];
+    out[t] = r;
+}
+
+}  // namespace
+
+extern "C" {
+
+int f2probe_copy(const uint64_t* src, uint64_t* dst, int64_t words, void* stream) {
+    if (words < 0 || (words > 0 && (!src || !dst)) || (words & 1) ||
+        (reinterpret_cast<uintptr_t>(src) & 15u) || (reinterpret_cast<uintptr_t>(dst) & 15u))
+        return -1;
+    if (words == 0) return 0;
+    const int64_t n16 = words / 2;
+    int64_t blocks = (n16 + kThreads - 1) / kThreads;
+    if (blocks > 256 * 32) blocks = 256 * 32;  // 32 workgroups per compute unit, then the loop
+    hipLaunchKernelGGL(k_probe_copy, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0,
+                       static_cast<hipStream_t>(stream), reinterpret_cast<const uint4*>(src),
+                       reinterpret_cast<uint4*>(dst), n16);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+int f2probe_bitops(uint32_t* out, int32_t blocks, int32_t iters, int32_t op, void* stream) {
+    if (!out || blocks < 1 || iters < 0 || (op != 0 && op != 1)) return -1;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (op == 0)
+        hipLaunchKernelGGL(k_probe_bitops<0>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, s, out, iters);
+    else
+        hipLaunchKernelGGL(k_probe_bitops<1>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, s, out, iters);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+}  // extern "C"

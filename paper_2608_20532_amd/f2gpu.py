@@ -16,11 +16,12 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libf2gpu.so")
+# F2GPU_LIB may name another build of the same source (the host-sanitizer build of the CPU tests)
+LIB_PATH = os.environ.get("F2GPU_LIB") or os.path.join(_HERE, "libf2gpu.so")
 
 F2_OK, F2_EINVAL, F2_EWORKSPACE, F2_EDEVICE, F2_ETOOWIDE = 0, -1, -2, -3, -4
 F2_MAX_N_BITS = 4095
-CTX_CONTRADICTION, CTX_BAD_SEGMENT, CTX_BAD_WIDTH, CTX_BAD_OUTPUT = 1, 2, 4, 8
+CTX_CONTRADICTION, CTX_BAD_SEGMENT, CTX_BAD_WIDTH, CTX_BAD_OUTPUT, CTX_SYNC_TIMEOUT = 1, 2, 4, 8, 16
 Q_OUT_OF_SPAN, Q_CTX_CONTRADICTORY, Q_BAD_CTX = 1, 2, 4
 POOL_SHARED, POOL_CONTRADICTION, POOL_WIDTH_MISMATCH, POOL_MASK_MISMATCH, POOL_BAD_MEMBER = 1, 2, 4, 8, 16
 

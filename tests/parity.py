@@ -106,3 +106,73 @@ def compare_encode(words_dev, qf_dev, ref_words, ref_qf, sample=None):
     assert np.array_equal(q, ref_qf), f"qflags differ at {np.count_nonzero(q != ref_qf)} queries"
     bad = np.nonzero((w != ref_words).any(axis=1))[0]
     assert len(bad) == 0, f"words differ at {len(bad)} queries, first {bad[:5]}"
+
+
+def _threads():
+    import os
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def oracle_fit_threads(rows, row_off, n_bits, threads=None) -> "oracle.FitResult":
+    """oracle.fit_batch over context ranges on several host threads (the single-threaded C
+    oracle releases the GIL; each range writes its own slice of the shared output arrays at
+    the documented offsets), for full-size workloads."""
+    import ctypes
+    from concurrent.futures import ThreadPoolExecutor
+    L = oracle.lib()
+    rows = np.ascontiguousarray(rows, np.uint64)
+    row_off = np.ascontiguousarray(row_off, np.int64)
+    n_bits = np.ascontiguousarray(n_bits, np.int32)
+    C = len(n_bits)
+    nb = np.clip(n_bits, 0, oracle.MAX_N)
+    bo, po, mo = oracle.layout(nb)
+    basis = np.zeros(max(int(bo[-1]), 1), np.uint64)
+    pivots = np.full(max(int(po[-1]), 1), -1, np.int32)
+    maps = np.zeros(max(int(mo[-1]), 1), np.uint64)
+    rank = np.zeros(C, np.int32)
+    flags = np.zeros(C, np.uint32)
+    n_contra = np.zeros(C, np.int32)
+    first = np.full(C, -1, np.int64)
+    # ranges of about equal row words
+    T = threads or _threads()
+    cuts = np.searchsorted(row_off, np.linspace(0, row_off[-1], 4 * T + 1)[1:-1]).tolist()
+    bounds = sorted(set([0] + [min(max(c, 0), C) for c in cuts] + [C]))
+
+    def addr(a, k):
+        return ctypes.c_void_p(a.ctypes.data + k * a.itemsize)
+
+    def run(c0, c1):
+        L.oracle_fit_batch(addr(rows, 0), rows.size, addr(row_off, c0), addr(n_bits, c0), c1 - c0,
+                           addr(bo, c0), int(bo[-1]), addr(po, c0), int(po[-1]), addr(mo, c0), int(mo[-1]),
+                           addr(basis, 0), addr(pivots, 0), addr(maps, 0), addr(rank, c0), addr(flags, c0),
+                           addr(n_contra, c0), addr(first, c0))
+
+    with ThreadPoolExecutor(T) as ex:
+        list(ex.map(lambda b: run(*b), [(a, b) for a, b in zip(bounds[:-1], bounds[1:]) if b > a]))
+    return oracle.FitResult(n_bits, bo, po, mo, basis, pivots, maps, rank, flags, n_contra, first)
+
+
+def oracle_encode_threads(ref: "oracle.FitResult", ctx_id, x, stride, threads=None):
+    """oracle.encode_batch over query ranges on several host threads; same outputs."""
+    from concurrent.futures import ThreadPoolExecutor
+    ctx_id = np.ascontiguousarray(ctx_id, np.int32)
+    x = np.ascontiguousarray(x, np.uint64)
+    Q = len(ctx_id)
+    T = threads or _threads()
+    step = max(1, -(-Q // (4 * T)))
+    parts = [(a, min(Q, a + step)) for a in range(0, Q, step)]
+    words = np.zeros((Q, 2), np.uint64)
+    qf = np.zeros(Q, np.uint8)
+
+    def run(a, b):
+        w, q = oracle.encode_batch(ref, ctx_id[a:b], x[a * stride:b * stride], stride)
+        words[a:b] = w
+        qf[a:b] = q
+
+    with ThreadPoolExecutor(T) as ex:
+        list(ex.map(lambda p: run(*p), parts))
+    return words, qf

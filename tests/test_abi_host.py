@@ -13,10 +13,10 @@ import oracle
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def declared_functions():
-    src = open(os.path.join(ROOT, "include", "f2gpu.h")).read()
+def declared_functions(header="f2gpu.h", prefix="f2_"):
+    src = open(os.path.join(ROOT, "include", header)).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(f2_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(" + prefix + r"[a-z_0-9]+)\s*\(", src)))
 
 
 def test_library_exports_every_declared_symbol():
@@ -27,6 +27,20 @@ def test_library_exports_every_declared_symbol():
     for name in names:
         assert hasattr(L, name), name
     assert set(f2gpu.EXPORTS) == set(names)
+
+
+def test_probe_library_exports_every_declared_symbol():
+    from paper_2608_20532_amd import f2probe
+    names = declared_functions("f2probe.h", "f2probe_")
+    assert len(names) == 2
+    L = ctypes.CDLL(f2probe.LIB_PATH)
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(f2probe.EXPORTS) == set(names)
+    # argument errors return before any device work
+    assert L.f2probe_copy(None, None, 4, None) == -1
+    assert L.f2probe_copy(None, None, 0, None) == 0
+    assert L.f2probe_bitops(None, 1, 1, 0, None) == -1
 
 
 def test_layout_matches_documented_capacities():

@@ -1,9 +1,11 @@
 """GPU parity: the HIP library against the CPU oracle, bit for bit, through the C ABI.
 
-Workloads: the four fit recipes at full size (recipe 4 on a subset of its 64
-identical-shape contexts), random batches covering every feature-word count
-1..64 with rank-deficient and contradictory data, the degenerate contexts the
-method has, and the query streams of the encode recipes.
+Workloads: the four fit recipes at full size (all 64 contexts of the wide
+recipe), random batches covering every feature-word count 1..64 with
+rank-deficient and contradictory data, the degenerate contexts the method has,
+and the query streams of the encode recipes, the 100M-query streams compared
+query by query.  Full-size workloads run the oracle on several host threads
+(context or query ranges; the oracle itself is single-threaded).
 """
 import numpy as np
 import pytest
@@ -23,13 +25,13 @@ def f2(require_gpu):
 
 def _fit_and_compare(f2, wl):
     print(f"fit parity: recipe {wl.recipe}, {wl.num_ctx} contexts, {wl.total_rows} rows", flush=True)
-    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    ref = parity.oracle_fit_threads(wl.rows, wl.row_off, wl.n_bits)
     model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
     parity.compare_fit(model, ref)
     return model, ref
 
 
-@pytest.mark.parametrize("recipe,num_ctx", [(1, 1), (2, 4096), (3, 80000), (4, 2)])
+@pytest.mark.parametrize("recipe,num_ctx", [(1, 1), (2, 4096), (3, 80000), (4, 64)])
 def test_fit_recipes(f2, recipe, num_ctx):
     wl = synth.fit_workload(recipe, num_ctx=num_ctx)
     model, ref = _fit_and_compare(f2, wl)
@@ -138,6 +140,36 @@ def test_fit_large_long_contexts(f2):
     full = ref.rank == np.array([n + 1 for n in n_bits])
     assert full.sum() >= 4 and (~full).sum() >= 4        # both regimes exercised
     assert ((ref.flags & 1) != 0).sum() >= 6            # contradictions found
+
+
+def test_group_barrier_timeout_is_reported(f2, monkeypatch):
+    """A few wide contexts, each fitted by a group of workgroups that exchange partial
+    sums across a bounded wait.  With the wait bound forced to zero from the host
+    (F2GPU_GROUP_SPIN_LIMIT=0: every wait gives up at once) every kernel still
+    finishes, every such context comes back flagged F2_CTX_SYNC_TIMEOUT, and its
+    queries are reported as bad contexts; with the default bound the same batch
+    matches the oracle and carries no such flag."""
+    import torch
+    rng = np.random.default_rng(91)
+    n_bits, rows_list = [], []
+    for k in range(8):
+        n = int(rng.integers(600, 1200))
+        n_bits.append(n)
+        rows_list.append(_large_context(rng, n, 300, "uniform" if k % 2 else "pool"))
+    wl = synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+    monkeypatch.setenv("F2GPU_GROUP_SPIN_LIMIT", "0")
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    flags = parity.host(model.ctx_flags, np.uint32)[:wl.num_ctx]
+    assert ((flags & f2.CTX_SYNC_TIMEOUT) != 0).all(), flags
+    ctx = np.repeat(np.arange(wl.num_ctx, dtype=np.int32), 16)
+    x = np.zeros(len(ctx) * 16, np.uint64)
+    words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x), 16)
+    torch.cuda.synchronize()
+    assert (parity.host(qf, np.uint8) == oracle.Q_BAD_CTX).all()
+    assert not parity.host(words, np.uint64).any()
+    monkeypatch.delenv("F2GPU_GROUP_SPIN_LIMIT")
+    model2, ref = _fit_and_compare(f2, wl)
+    assert not (parity.host(model2.ctx_flags, np.uint32)[:wl.num_ctx] & f2.CTX_SYNC_TIMEOUT).any()
 
 
 @pytest.mark.parametrize("num_ctx", [100, 200])
@@ -367,15 +399,34 @@ def test_encode_random_widths_and_bad_ids(f2):
     assert (rq & oracle.Q_OUT_OF_SPAN).any() and (rq == 0).any() and (rq & oracle.Q_BAD_CTX).any()
 
 
-def test_encode_recipe5_full_size_sampled(f2):
-    """The 100M-query Zipf stream at full size; the oracle checks a random sample of 200k queries."""
+def _encode_full_size(f2, wl, nq, stride, frac, zipf):
+    """Fit a full-size workload on the GPU (checked against the oracle), encode a
+    full-size query stream against it and compare every word and flag."""
+    import torch
+    model, ref = _fit_and_compare(f2, wl)
+    ctx, x, planted = synth.queries(wl, nq, stride, frac, zipf)
+    print(f"encode parity: {nq} queries, stride {stride}, all compared", flush=True)
+    words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x), stride)
+    torch.cuda.synchronize()
+    rw, rq = parity.oracle_encode_threads(ref, ctx, x, stride)
+    parity.compare_encode(words, qf, rw, rq)
+    assert abs(planted.mean() - frac) < 0.2 * frac
+    return rq
+
+
+def test_encode_recipe5_full_size(f2):
+    """The 100M-query Zipf stream of the encode recipe at full size, every query compared."""
     wl = synth.fit_workload(5)
-    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
-    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
     nq, stride, frac, zipf = synth.QUERY_RECIPE[5]
-    sample = np.sort(np.random.default_rng(1).choice(nq, size=200_000, replace=False))
-    planted = _encode_and_compare(f2, wl, model, ref, nq, stride, frac, zipf, sample=sample)
-    assert 0.008 < planted.mean() < 0.012
+    rq = _encode_full_size(f2, wl, nq, stride, frac, zipf)
+    assert 0.008 < ((rq & oracle.Q_OUT_OF_SPAN) != 0).mean() < 0.012
+
+
+def test_bench_step_full_size(f2):
+    """The benchmark's default step exactly: the 80,000-context fit, then 100M Zipf queries
+    (stride 4, 1% out of span) against the maps just fitted, every output compared."""
+    wl = synth.fit_workload(3)
+    _encode_full_size(f2, wl, 100_000_000, 4, 0.01, 1.1)
 
 
 @pytest.mark.parametrize("stride", [3, 1, 7])
