@@ -470,6 +470,56 @@ def test_encode_grouped_path_random_widths(f2, stride):
     assert (rq == 0).sum() > 1000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 1000 and (rq & oracle.Q_BAD_CTX).any()
 
 
+@pytest.mark.parametrize("stride", [1, 2, 5])
+def test_encode_large_batch_random_widths(f2, stride):
+    """A batch above 4,194,304 queries (x words carried through the sort, nibble-table
+    sorted pass for contexts of 1-127 bits, per-lane pass for wider ones and n = 0)
+    over every width class, with in-span queries, single-bit flips inside and outside
+    the width, junk words and ids out of range; every query compared."""
+    import torch
+    rng = np.random.default_rng(100 + stride)
+    widths = list(rng.integers(1, 140, size=300)) + [0, 0, 1, 2, 3, 62, 63, 64, 65, 126, 127, 128, 129, 255, 256,
+                                                     300, 511, 600, 4095]
+    wl = _random_batch(200 + stride, widths, max_rows=160)
+    ref = parity.oracle_fit_threads(wl.rows, wl.row_off, wl.n_bits)
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    C = wl.num_ctx
+    # a pool of 8 candidate x per context: XOR of 1-3 training rows, the constant and padding dropped
+    pool = np.zeros((C, 8, stride), np.uint64)
+    for c in range(C):
+        n = int(wl.n_bits[c]); fw = (n + 64) // 64; m = int(wl.m_rows[c])
+        if m == 0:
+            continue
+        rows_c = wl.rows[wl.row_off[c]:wl.row_off[c + 1]].reshape(-1, fw + 2)
+        for k in range(8):
+            sel = rows_c[rng.integers(0, m, size=int(rng.integers(1, 4)))]
+            v = np.bitwise_xor.reduce(sel[:, :fw], axis=0)
+            for w in range(min(fw, stride)):
+                lo = 64 * w
+                keep = min(max(n - lo, 0), 64)
+                pool[c, k, w] = v[w] & np.uint64((1 << keep) - 1)
+    nq = 4_500_000
+    ctx = rng.integers(-2, C + 2, size=nq).astype(np.int32)
+    ok = (ctx >= 0) & (ctx < C)
+    cc = np.where(ok, ctx, 0)
+    x = pool[cc, rng.integers(0, 8, size=nq)].copy()
+    mode = rng.integers(0, 10, size=nq)
+    # mode 0-1: one random bit of the stride flipped (inside or outside the width); 2: junk; else as drawn
+    flip = np.nonzero(mode <= 1)[0]
+    b = rng.integers(0, 64 * stride, size=len(flip))
+    x[flip, b // 64] ^= np.uint64(1) << (b % 64).astype(np.uint64)
+    junk = np.nonzero(mode == 2)[0]
+    x[junk] = rng.integers(0, 2 ** 63, size=(len(junk), stride), dtype=np.uint64) >> rng.integers(0, 64, size=(len(junk), 1)).astype(np.uint64)
+    x = x.reshape(-1)
+    print(f"large-batch encode parity: {nq} queries, stride {stride}, {C} contexts", flush=True)
+    words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x), stride)
+    torch.cuda.synchronize()
+    rw, rq = parity.oracle_encode_threads(ref, ctx, x, stride)
+    parity.compare_encode(words, qf, rw, rq)
+    assert (rq == 0).sum() > 300_000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 500_000
+    assert (rq & oracle.Q_BAD_CTX).sum() > 10_000 and (rq & oracle.Q_CTX_CONTRADICTORY).any()
+
+
 def _bad_context_model(f2):
     """40 contexts of recipe 2's shape with two malformed ones (1: too wide; 3: a segment
     that is not a whole number of rows), fitted on the GPU; returns (wl, oracle fit, model)."""
