@@ -54,7 +54,8 @@ typedef enum {
     F2_EINVAL = -1,      /* null pointer, negative count, bad stride, ... */
     F2_EWORKSPACE = -2,  /* workspace missing or smaller than required */
     F2_EDEVICE = -3,     /* HIP error while enqueuing */
-    F2_ETOOWIDE = -4     /* host-side layout helper: a width above F2_MAX_N_BITS */
+    F2_ETOOWIDE = -4,    /* host-side layout helper: a width above F2_MAX_N_BITS */
+    F2_ESCRATCH = -5     /* f2_fit_batch_noalloc: more contexts than F2_NOALLOC_MAX_CTX */
 } f2_status;
 
 #define F2_MAX_N_BITS 4095 /* widest supported context: fw <= 64 feature words */
@@ -156,6 +157,23 @@ size_t f2_fit_workspace_bytes(int32_t num_ctx);
  */
 int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* model_host,
                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): f2_fit_batch without a
+ * workspace.  The per-batch plan lives in a fixed device array of the library
+ * (about 1.5 MB on each device the library runs on, held until the process
+ * ends), so the call allocates nothing; inputs, outputs and semantics are those
+ * of f2_fit_batch.  Every call on a device shares that device's array: calls
+ * that overlap on one device (concurrent streams, threads) race and must be
+ * serialised by the caller.  The array's address is looked up on the first call
+ * on each device.
+ * Returns F2_OK, F2_EINVAL, F2_ESCRATCH (more than F2_NOALLOC_MAX_CTX contexts:
+ * nothing enqueued) or F2_EDEVICE.
+ */
+#define F2_NOALLOC_MAX_CTX 131072
+int f2_fit_batch_noalloc(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* model_host,
+                         void* stream);
 
 /*
  * Workspace bytes f2_encode_batch needs for a fitted model and a batch size

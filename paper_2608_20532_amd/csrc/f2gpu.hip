@@ -3534,6 +3534,7 @@ const char* f2_status_string(int status) {
         case F2_EWORKSPACE: return "workspace missing or too small";
         case F2_EDEVICE: return "HIP error while enqueuing device work";
         case F2_ETOOWIDE: return "context width above F2_MAX_N_BITS";
+        case F2_ESCRATCH: return "batch above the allocation-free fit's fixed plan size (F2_NOALLOC_MAX_CTX contexts)";
         default: return "unknown status";
     }
 }
@@ -3565,6 +3566,60 @@ size_t f2_fit_workspace_bytes(int32_t num_ctx) {
     if (num_ctx < 0) return 0;
     const size_t blocks = (static_cast<size_t>(num_ctx) + kPlanThreads - 1) / kPlanThreads;
     return align256(sizeof(int32_t) * (kPlanHead + 2 * static_cast<size_t>(num_ctx) + kPlanBins * blocks));
+}
+
+}  // extern "C"
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// allocation-free fit: the plan lives in a fixed device array instead of a
+// caller workspace.  The array's name is a host-side stand-in; its device address
+// is looked up once per device (hipGetSymbolAddress with that device current)
+// and kept, and only that address is handed to kernels.  Every call on a device
+// shares its array: calls that overlap on one device race.  The plan kernels
+// initialise every plan word they read, so nothing stale carries over.
+// ---------------------------------------------------------------------------
+constexpr int32_t kScratchMaxCtx = F2_NOALLOC_MAX_CTX;
+constexpr size_t kScratchBytes =
+    (sizeof(int32_t) * (kPlanHead + 2 * static_cast<size_t>(kScratchMaxCtx) +
+                        kPlanBins * ((static_cast<size_t>(kScratchMaxCtx) + kPlanThreads - 1) / kPlanThreads)) +
+     255) / 256 * 256;
+constexpr int kScratchDevices = 64;
+
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+// device address of this device's scratch array, or nullptr if it cannot be found
+void* scratch_address() {
+    static std::atomic<void*> addr[kScratchDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return nullptr;
+    void* p = addr[dev].load(std::memory_order_acquire);
+    if (p) return p;
+    void* q = nullptr;
+    if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    addr[dev].store(q, std::memory_order_release);  // the same address whichever thread looks it up
+    return q;
+}
+
+}  // namespace
+
+extern "C" {
+
+int f2_fit_batch_noalloc(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m,
+                         void* stream) {
+    if (!m || m->num_ctx < 0 || rows_words < 0) return F2_EINVAL;
+    const int32_t C = m->num_ctx;
+    if (C == 0) return F2_OK;
+    if (!row_off || !model_complete(m) || (rows_words > 0 && !rows)) return F2_EINVAL;
+    if (C > kScratchMaxCtx || f2_fit_workspace_bytes(C) > kScratchBytes) return F2_ESCRATCH;
+    void* plan = scratch_address();
+    if (!plan) return F2_EDEVICE;
+    launch_fit(fit_args(rows, rows_words, row_off, m, static_cast<int32_t*>(plan)), static_cast<hipStream_t>(stream));
+    return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 
 int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m,

@@ -19,14 +19,15 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 # F2GPU_LIB may name another build of the same source (the host-sanitizer build of the CPU tests)
 LIB_PATH = os.environ.get("F2GPU_LIB") or os.path.join(_HERE, "libf2gpu.so")
 
-F2_OK, F2_EINVAL, F2_EWORKSPACE, F2_EDEVICE, F2_ETOOWIDE = 0, -1, -2, -3, -4
+F2_OK, F2_EINVAL, F2_EWORKSPACE, F2_EDEVICE, F2_ETOOWIDE, F2_ESCRATCH = 0, -1, -2, -3, -4, -5
+F2_NOALLOC_MAX_CTX = 131072
 F2_MAX_N_BITS = 4095
 CTX_CONTRADICTION, CTX_BAD_SEGMENT, CTX_BAD_WIDTH, CTX_BAD_OUTPUT, CTX_SYNC_TIMEOUT = 1, 2, 4, 8, 16
 Q_OUT_OF_SPAN, Q_CTX_CONTRADICTORY, Q_BAD_CTX = 1, 2, 4
 POOL_SHARED, POOL_CONTRADICTION, POOL_WIDTH_MISMATCH, POOL_MASK_MISMATCH, POOL_BAD_MEMBER = 1, 2, 4, 8, 16
 
 # every entry point the header declares
-EXPORTS = ("f2_fit_layout", "f2_fit_workspace_bytes", "f2_fit_batch", "f2_encode_workspace_bytes",
+EXPORTS = ("f2_fit_layout", "f2_fit_workspace_bytes", "f2_fit_batch", "f2_fit_batch_noalloc", "f2_encode_workspace_bytes",
            "f2_encode_batch", "f2_vectorize_rows", "f2_merge_words", "f2_pool_workspace_bytes", "f2_pool_bases",
            "f2_group_workspace_bytes", "f2_group_rows", "f2_status_string")
 
@@ -65,6 +66,8 @@ def _load():
     L.f2_fit_workspace_bytes.restype = sz
     L.f2_fit_batch.argtypes = [P, i64, P, MP, P, sz, P]
     L.f2_fit_batch.restype = ctypes.c_int
+    L.f2_fit_batch_noalloc.argtypes = [P, i64, P, MP, P]
+    L.f2_fit_batch_noalloc.restype = ctypes.c_int
     L.f2_encode_workspace_bytes.argtypes = [MP, i64]
     L.f2_encode_workspace_bytes.restype = sz
     L.f2_encode_batch.argtypes = [MP, P, P, i32, i64, P, P, P, sz, P]
@@ -171,6 +174,12 @@ def f2_fit_batch(rows, rows_words: int, row_off, model: Model, workspace, worksp
     """Enqueue the fit of every context; returns the status code."""
     return int(lib.f2_fit_batch(_ptr(rows), int(rows_words), _ptr(row_off), ctypes.byref(model.struct()),
                                 _ptr(workspace), int(workspace_bytes), _stream(stream)))
+
+
+def f2_fit_batch_noalloc(rows, rows_words: int, row_off, model: Model, stream=None) -> int:
+    """Enqueue the fit without a workspace (the plan in the library's fixed device array); returns the status."""
+    return int(lib.f2_fit_batch_noalloc(_ptr(rows), int(rows_words), _ptr(row_off), ctypes.byref(model.struct()),
+                                        _stream(stream)))
 
 
 def f2_encode_batch(model: Model, ctx_id, x, x_stride_words: int, num_queries: int, words_out, qflags_out,

@@ -63,7 +63,7 @@ def test_layout_errors():
 
 def test_status_strings_and_workspace_sizes():
     from paper_2608_20532_amd import f2gpu
-    for st in (0, -1, -2, -3, -4):
+    for st in (0, -1, -2, -3, -4, -5):
         assert f2gpu.f2_status_string(st) != "unknown status"
     assert f2gpu.f2_status_string(7) == "unknown status"
     assert f2gpu.f2_fit_workspace_bytes(-1) == 0
@@ -117,3 +117,22 @@ def test_vectorize_and_merge_argument_errors():
     assert M(None, None, 0, 0, (0, 0), None, 3, None, 0) == f2gpu.F2_EINVAL
     assert M(f, None, 0, 0, (0, 0), None, -2, f, 0) == f2gpu.F2_EINVAL
     assert f2gpu.lib.f2_merge_words(None, None, 0, 0, None, None, 0, None, None) == f2gpu.F2_EINVAL
+
+
+def test_noalloc_fit_rejects_batches_beyond_its_fixed_plan():
+    """The allocation-free fit refuses more contexts than its fixed plan holds, and bad
+    arguments, before any device work."""
+    from paper_2608_20532_amd import f2gpu
+    m = f2gpu.f2_model()
+    for name in ("n_bits", "basis_off", "piv_off", "map_off", "basis", "pivots", "maps", "tables", "rank",
+                 "ctx_flags", "n_contra", "first_contra_row"):
+        setattr(m, name, 256)
+    m.num_ctx = f2gpu.F2_NOALLOC_MAX_CTX + 1
+    L = f2gpu.lib
+    assert L.f2_fit_batch_noalloc(256, 0, 256, ctypes.byref(m), None) == f2gpu.F2_ESCRATCH
+    assert "allocation-free" in f2gpu.f2_status_string(f2gpu.F2_ESCRATCH)
+    m.num_ctx = 0
+    assert L.f2_fit_batch_noalloc(None, 0, None, ctypes.byref(m), None) == f2gpu.F2_OK
+    m.num_ctx = 5
+    assert L.f2_fit_batch_noalloc(None, 0, None, ctypes.byref(m), None) == f2gpu.F2_EINVAL
+    assert L.f2_fit_batch_noalloc(None, 0, None, None, None) == f2gpu.F2_EINVAL
