@@ -33,8 +33,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# integer VALU peak: 256 compute units x 64 lanes x 2.4 GHz, one 32-bit lane operation each
-INT_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+# integer VALU peak: the fp32 vector rate (157.3 TFLOP/s = 256 compute units x 2.4 GHz x 256
+# flops) counts an FMA as two flops, so a compute unit retires 128 32-bit lane operations per
+# clock; bitwise ops issue at that rate (the probe's v_xor_b32 run reaches 54.8 T/s, above the
+# 39.3 T/s that 64 lanes per clock would allow)
+INT_PEAK_TOPS = 256 * 128 * 2.4e9 / 1e12
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_20532_amd", "csrc", "f2gpu.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
 
@@ -437,7 +440,7 @@ def measured_ceilings(stream):
     import torch
     from paper_2608_20532_amd import f2probe
     dev = torch.device("cuda:0")
-    words = (1 << 30) // 8  # 1 GiB each way
+    words = (1 << 31) // 8  # 2 GiB each way
     src = torch.ones(words, dtype=torch.int64, device=dev)
     dst = torch.empty_like(src)
     out = torch.empty(256 * 256 * 8, dtype=torch.int32, device=dev)

@@ -1,5 +1,5 @@
 // f2probe.hip -- ceiling probes for the roofline figures (gfx950): a streaming
-// copy (achievable HBM bandwidth) and a run of independent 32-bit bitwise VALU
+// non-temporal copy (achievable HBM bandwidth) and a run of independent 32-bit bitwise VALU
 // instructions (achievable integer issue rate).  Nothing here is part of the
 // fit or the encode.
 #include <hip/hip_runtime.h>
@@ -11,19 +11,23 @@ namespace {
 
 constexpr int kThreads = 256;
 
-__global__ __launch_bounds__(kThreads) void k_probe_copy(const uint4* __restrict__ src, uint4* __restrict__ dst,
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// non-temporal 16-byte loads and stores (the streamed data is not kept in the
+// caches), four in flight per thread, a grid-stride loop
+__global__ __launch_bounds__(kThreads) void k_probe_copy(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
                                                          int64_t n16) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
     int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
-    // four independent 16-byte loads in flight per thread, then their stores
     for (; i + 3 * stride < n16; i += 4 * stride) {
-        const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
-        dst[i] = a;
-        dst[i + stride] = b;
-        dst[i + 2 * stride] = c;
-        dst[i + 3 * stride] = d;
+        const u32x4 a = __builtin_nontemporal_load(src + i), b = __builtin_nontemporal_load(src + i + stride);
+        const u32x4 c = __builtin_nontemporal_load(src + i + 2 * stride), d = __builtin_nontemporal_load(src + i + 3 * stride);
+        __builtin_nontemporal_store(a, dst + i);
+        __builtin_nontemporal_store(b, dst + i + stride);
+        __builtin_nontemporal_store(c, dst + i + 2 * stride);
+        __builtin_nontemporal_store(d, dst + i + 3 * stride);
     }
-    for (; i < n16; i += stride) dst[i] = src[i];
+    for (; i < n16; i += stride) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
 }
 
 constexpr int kVals = 16;
@@ -60,10 +64,10 @@ int f2probe_copy(const uint64_t* src, uint64_t* dst, int64_t words, void* stream
     if (words == 0) return 0;
     const int64_t n16 = words / 2;
     int64_t blocks = (n16 + kThreads - 1) / kThreads;
-    if (blocks > 256 * 32) blocks = 256 * 32;  // 32 workgroups per compute unit, then the loop
+    if (blocks > 131072) blocks = 131072;  // then the loop (fastest of 2k-128k workgroups on 2 GiB)
     hipLaunchKernelGGL(k_probe_copy, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0,
-                       static_cast<hipStream_t>(stream), reinterpret_cast<const uint4*>(src),
-                       reinterpret_cast<uint4*>(dst), n16);
+                       static_cast<hipStream_t>(stream), reinterpret_cast<const u32x4*>(src),
+                       reinterpret_cast<u32x4*>(dst), n16);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
