@@ -569,6 +569,11 @@ def phases_and_roofline(name, wl, nq, stride, do_fit, fit_ms, enc_ms, rank, ceil
             roof["frac_of_measured_peak"] = phases[dom]["GBps"] / ceil["copy_GBps"]
     if tr:
         roof["kernels"] = tr["kernels"]
+        # the bytes the counters saw crossing to the fabric, at the call's measured time
+        roof["traffic_GBps"] = tr["bytes"] / (phases[dom]["ms"] * 1e-3) / 1e9
+        roof["traffic_over_algorithmic"] = tr["bytes"] / phases[dom]["bytes"]
+        if ceil:
+            roof["traffic_frac_of_measured_peak"] = roof["traffic_GBps"] / ceil["copy_GBps"]
     else:
         roof["traffic_note"] = why or f"no counters for the {dom} phase of this workload"
     return phases, roof

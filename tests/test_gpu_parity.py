@@ -632,3 +632,59 @@ def test_fit_long_high_rank_contexts(f2):
     whose positions outrun the tables too (d = 256)."""
     widths = [100, 130, 150, 191, 200, 230, 250, 255, 254, 180, 120, 240]
     _fit_and_compare(f2, _late_pivot_batch(57, widths, [1100, 1800, 3000], kmax=256))
+
+
+def _subspace_rows(rng, n, m, k, contra_rows=(), grow_rows=()):
+    """m rows of width n whose features come from a k-dimensional subspace (random
+    generators, constant bit included as drawn), outputs linear in the generators;
+    the listed rows get a flipped output bit (contradictions) or a fresh random
+    feature vector (a new pivot, unless it happens to lie in the span)."""
+    fw = (n + 64) // 64
+    d = n + 1
+    vb = d - 64 * (fw - 1)
+    top = np.uint64(((1 << vb) - 1) if vb < 64 else (1 << 64) - 1)
+    pool = rng.integers(0, 2 ** 63, size=(k, fw), dtype=np.uint64) ^ (rng.integers(0, 2, size=(k, fw), dtype=np.uint64) << np.uint64(63))
+    pool[:, fw - 1] &= top
+    Wp = rng.integers(0, 2 ** 63, size=(k, 2), dtype=np.uint64)
+    rows = np.zeros((m, fw + 2), np.uint64)
+    sel = rng.integers(0, 2, size=(m, k)).astype(bool)
+    for i in range(m):
+        rows[i, :fw] = np.bitwise_xor.reduce(pool[sel[i]], axis=0) if sel[i].any() else 0
+        rows[i, fw:] = np.bitwise_xor.reduce(Wp[sel[i]], axis=0) if sel[i].any() else 0
+    for i in contra_rows:
+        rows[i, fw] ^= np.uint64(1) << np.uint64(int(rng.integers(0, 64)))
+    for i in grow_rows:
+        rows[i, :fw] = rng.integers(0, 2 ** 63, size=fw, dtype=np.uint64) ^ (rng.integers(0, 2, size=fw, dtype=np.uint64) << np.uint64(63))
+        rows[i, fw - 1] &= top
+        rows[i, fw:] = rng.integers(0, 2 ** 63, size=2, dtype=np.uint64)
+    return rows
+
+
+def test_fit_late_rows_after_saturation(f2):
+    """Long contexts at every width class (one to eight feature words), of full rank
+    and of low rank (rank below d / 2), whose rank saturates early: contradictions
+    only long after saturation (counted, first row kept), a new pivot at the very
+    last row, one deep inside the stream, one right after the first blocks of 64,
+    and a contradiction among the first rows.  More than 64 contexts, so the
+    planned path (class lists, LDS-basis and register kernels) runs."""
+    rng = np.random.default_rng(2026)
+    cases = []
+    for n in (20, 40, 63, 100, 150, 191, 200, 255, 300, 447, 511):
+        d = n + 1
+        for k in (max(1, d // 8), min(d, int(0.7 * d) + 1)):
+            cases.append((n, 3 * d + 400, k, (3 * d + 100, 3 * d + 101, 3 * d + 399), ()))   # contradictions late
+            cases.append((n, 3 * d + 400, k, (5,), (3 * d + 399,)))                           # new pivot at the end
+            cases.append((n, 2 * d + 300, k, (), (2 * d + 150,)))                             # new pivot mid-suffix
+        cases.append((n, d + 700, min(d, 30), (d + 650,), (64 * ((d + 95) // 64),)))           # right after the first blocks
+    n_bits, rows_list = [], []
+    for (n, m, k, contra, grow) in cases:
+        n_bits.append(n)
+        rows_list.append(_subspace_rows(rng, n, m, k, contra, grow))
+    # filler contexts: more than the small-batch bound, so the planned path runs
+    for i in range(80):
+        n = int(rng.integers(0, 200))
+        n_bits.append(n)
+        rows_list.append(_subspace_rows(rng, n, int(rng.integers(0, 300)), int(rng.integers(1, n + 2))))
+    wl = synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
+    model, ref = _fit_and_compare(f2, wl)
+    assert (ref.n_contra[:len(cases)] > 0).sum() >= 20
