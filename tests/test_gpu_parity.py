@@ -688,3 +688,68 @@ def test_fit_late_rows_after_saturation(f2):
     wl = synth.custom_workload(n_bits, [len(r) for r in rows_list], rows_list)
     model, ref = _fit_and_compare(f2, wl)
     assert (ref.n_contra[:len(cases)] > 0).sum() >= 20
+
+
+def _ctx_outputs(h, model, i):
+    """Every output of context i of a fitted model (host copy h), independent of its position in the batch."""
+    r = int(h["rank"][i])
+    n = int(h["n_bits"][i])
+    fw = (n + 64) // 64
+    W = fw + 2
+    bo, po, mo = int(model.basis_off_host[i]), int(model.piv_off_host[i]), int(model.map_off_host[i])
+    t = (n + 1) - r
+    tables = h["tables"][bo:bo + t * fw] if t <= r else np.zeros(0, np.uint64)
+    return (r, int(h["flags"][i]), int(h["n_contra"][i]), int(h["first"][i]),
+            h["basis"][bo:bo + r * W].tobytes(), h["pivots"][po:po + r].tobytes(),
+            h["maps"][mo:mo + 2 * (n + 1)].tobytes(), tables.tobytes())
+
+
+def _fit_subset(f2, wl, order):
+    """Fit the contexts of wl in the given order (a list of context indices) as one batch."""
+    rows = [wl.rows[wl.row_off[c]:wl.row_off[c + 1]].reshape(-1, (int(wl.n_bits[c]) + 64) // 64 + 2) for c in order]
+    sub = synth.custom_workload(wl.n_bits[order], [len(r) for r in rows], rows)
+    model = parity.gpu_fit(f2, sub.rows, sub.row_off, sub.n_bits)
+    h = parity.model_to_host(model)
+    h["n_bits"] = np.asarray(sub.n_bits)
+    return model, h
+
+
+def test_fit_deterministic_across_launch_geometries(f2):
+    """The same contexts fitted under different launch geometries give identical outputs:
+    a batch of at most 64 contexts (one workgroup per context, no plan) against the same
+    contexts spread through a batch of 3,000 (plan, class kernels, different workgroups
+    and list positions); wide contexts fitted by groups of 4, 2 and 1 workgroups (alone,
+    among 100 and among 200 other wide contexts)."""
+    rng = np.random.default_rng(77)
+    widths = [int(w) for w in rng.integers(0, 512, size=36)] + [0, 63, 64, 511]
+    small = _random_batch(78, widths, max_rows=600)
+    filler = synth.fit_workload(3, num_ctx=3000)
+    # one workload holding both: the 40 targets first, then the filler contexts
+    rows = [small.rows[small.row_off[c]:small.row_off[c + 1]].reshape(-1, (int(small.n_bits[c]) + 64) // 64 + 2)
+            for c in range(small.num_ctx)]
+    rows += [filler.rows[filler.row_off[c]:filler.row_off[c + 1]].reshape(-1, (int(filler.n_bits[c]) + 64) // 64 + 2)
+             for c in range(filler.num_ctx)]
+    both = synth.custom_workload(list(small.n_bits) + list(filler.n_bits), [len(r) for r in rows], rows)
+    T = small.num_ctx
+    m1, h1 = _fit_subset(f2, both, list(range(T)))                      # small-batch kernel
+    pos = rng.permutation(both.num_ctx)                                 # targets at random list positions
+    m2, h2 = _fit_subset(f2, both, list(pos))
+    inv = np.argsort(pos)
+    for i in range(T):
+        assert _ctx_outputs(h1, m1, i) == _ctx_outputs(h2, m2, int(inv[i])), f"context {i} (n={widths[i]})"
+    ref = oracle.fit_batch(small.rows, small.row_off, small.n_bits)
+    parity.compare_fit(m1, ref)
+
+    # wide contexts: groups of 4 (alone), 2 (with 100 others) and 1 (with 200 others)
+    wide_rows, wide_n = [], []
+    for n, m, kind in ((700, 900, "uniform"), (1500, 400, "pool"), (2100, 2300, "mixed")):
+        wide_n.append(n)
+        wide_rows.append(_large_context(rng, n, m, kind))
+    fill_n = [512 + int(k) for k in rng.integers(0, 200, size=200)]
+    fill_rows = [_large_context(rng, n, 40, "pool") for n in fill_n]
+    allw = synth.custom_workload(wide_n + fill_n, [len(r) for r in wide_rows + fill_rows], wide_rows + fill_rows)
+    outs = []
+    for extra in (0, 100, 200):
+        mw, hw = _fit_subset(f2, allw, list(range(3 + extra)))
+        outs.append([_ctx_outputs(hw, mw, i) for i in range(3)])
+    assert outs[0] == outs[1] == outs[2]
