@@ -178,6 +178,10 @@ int f2_fit_batch_noalloc(const uint64_t* rows, int64_t rows_words, const int64_t
 /*
  * Workspace bytes f2_encode_batch needs for a fitted model and a batch size
  * (scratch for the batch; the model's tables are part of the fit outputs).
+ * Batches above 2^30 queries are encoded in chunks of 2^30, so the workspace
+ * is that of one chunk.  The environment variable F2GPU_ENCODE_CHUNK, read at
+ * each call, may set a smaller chunk (1 .. 2^30; a test hook): the size must be
+ * the same when this is called and when f2_encode_batch runs.
  */
 size_t f2_encode_workspace_bytes(const f2_model* model_host, int64_t num_queries);
 
@@ -191,6 +195,10 @@ size_t f2_encode_workspace_bytes(const f2_model* model_host, int64_t num_queries
  *   qflags_out [num_queries] F2_Q_* flags
  * A query with any x bit at or above its context's width n lies outside that
  * context's ambient space and is reported unsupported.
+ * The model must come from f2_fit_batch (or f2_pool_bases): the parity-check
+ * rows in tables are written by the fit.  A batch of more than one chunk (see
+ * f2_encode_workspace_bytes) is enqueued chunk after chunk on the stream; the
+ * results do not depend on the chunking.
  * Returns F2_OK, F2_EINVAL, F2_EWORKSPACE or F2_EDEVICE.
  */
 int f2_encode_batch(const f2_model* model_host, const int32_t* ctx_id, const uint64_t* x, int32_t x_stride_words,

@@ -3439,6 +3439,20 @@ int group_spin_limit() {
     return x > (1 << 24) ? (1 << 24) : static_cast<int>(x);
 }
 
+// queries per encode chunk: the grouped path indexes a batch's positions in 32
+// bits, so larger batches are encoded in chunks of 2^30 (each grouped on its own,
+// one after the other through one chunk-sized workspace); F2GPU_ENCODE_CHUNK may
+// set a smaller chunk (a test hook for the chunking)
+constexpr int64_t kEncChunk = int64_t{1} << 30;
+int64_t encode_chunk() {
+    const char* v = getenv("F2GPU_ENCODE_CHUNK");
+    if (!v || !*v) return kEncChunk;
+    char* end = nullptr;
+    const long long x = strtoll(v, &end, 10);
+    if (*end != '\0' || x < 1 || x > kEncChunk) return kEncChunk;
+    return x;
+}
+
 FitArgs fit_args(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m, int32_t* plan) {
     FitArgs a;
     a.rows = rows;
@@ -3637,22 +3651,17 @@ int f2_fit_batch(const uint64_t* rows, int64_t rows_words, const int64_t* row_of
 
 size_t f2_encode_workspace_bytes(const f2_model* m, int64_t num_queries) {
     if (!m || m->num_ctx < 0 || num_queries < 0) return 0;
-    return encode_workspace(m->num_ctx, num_queries).bytes;
+    const int64_t chunk = encode_chunk();
+    return encode_workspace(m->num_ctx, num_queries < chunk ? num_queries : chunk).bytes;
 }
 
-int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x, int32_t x_stride_words,
-                    int64_t num_queries, uint64_t* words_out, uint8_t* qflags_out, void* workspace,
-                    size_t workspace_bytes, void* stream) {
-    if (!m || m->num_ctx < 0 || num_queries < 0 || x_stride_words < 1) return F2_EINVAL;
-    if (num_queries == 0) return F2_OK;
-    if (!ctx_id || !x || !words_out || !qflags_out) return F2_EINVAL;
-    if (m->num_ctx > 0 && (!m->n_bits || !m->basis_off || !m->piv_off || !m->map_off || !m->basis || !m->pivots ||
-                           !m->maps || !m->tables || !m->rank || !m->ctx_flags))
-        return F2_EINVAL;
-    if (!workspace || workspace_bytes < f2_encode_workspace_bytes(m, num_queries) ||
-        (reinterpret_cast<uintptr_t>(workspace) & 255u))
-        return F2_EWORKSPACE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
+}  // extern "C"
+
+namespace {
+
+// one chunk of at most encode_chunk() queries (arguments checked by the caller)
+int encode_range(const f2_model* m, const int32_t* ctx_id, const uint64_t* x, int32_t x_stride_words,
+                 int64_t num_queries, uint64_t* words_out, uint8_t* qflags_out, void* workspace, hipStream_t s) {
     EncArgs e;
     e.num_ctx = m->num_ctx;
     e.n_bits = m->n_bits;
@@ -3707,6 +3716,34 @@ int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x,
     if (!p.s.direct)
         hipLaunchKernelGGL(k_enc_unsort, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
+}
+
+}  // namespace
+
+extern "C" {
+
+int f2_encode_batch(const f2_model* m, const int32_t* ctx_id, const uint64_t* x, int32_t x_stride_words,
+                    int64_t num_queries, uint64_t* words_out, uint8_t* qflags_out, void* workspace,
+                    size_t workspace_bytes, void* stream) {
+    if (!m || m->num_ctx < 0 || num_queries < 0 || x_stride_words < 1) return F2_EINVAL;
+    if (num_queries == 0) return F2_OK;
+    if (!ctx_id || !x || !words_out || !qflags_out) return F2_EINVAL;
+    if (m->num_ctx > 0 && (!m->n_bits || !m->basis_off || !m->piv_off || !m->map_off || !m->basis || !m->pivots ||
+                           !m->maps || !m->tables || !m->rank || !m->ctx_flags))
+        return F2_EINVAL;
+    if (!workspace || workspace_bytes < f2_encode_workspace_bytes(m, num_queries) ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u))
+        return F2_EWORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // chunks in stream order through the one workspace
+    const int64_t chunk = encode_chunk();
+    for (int64_t q0 = 0; q0 < num_queries; q0 += chunk) {
+        const int64_t n = num_queries - q0 < chunk ? num_queries - q0 : chunk;
+        const int st = encode_range(m, ctx_id + q0, x + q0 * x_stride_words, x_stride_words, n, words_out + 2 * q0,
+                                    qflags_out + q0, workspace, s);
+        if (st != F2_OK) return st;
+    }
+    return F2_OK;
 }
 
 int f2_vectorize_rows(const uint64_t* values, const uint64_t* y, int64_t num_rows, int32_t k,

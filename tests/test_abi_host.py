@@ -78,6 +78,21 @@ def test_status_strings_and_workspace_sizes():
     assert f2gpu.lib.f2_encode_workspace_bytes(ctypes.byref(m), -1) == 0
 
 
+def test_encode_workspace_is_one_chunk(monkeypatch):
+    """Batches above the chunk size are encoded chunk by chunk through one chunk-sized
+    workspace: 2^30 queries by default, less under F2GPU_ENCODE_CHUNK."""
+    from paper_2608_20532_amd import f2gpu
+    m = f2gpu.f2_model()
+    m.num_ctx, m.basis_words = 80_000, 1000
+    ws = lambda q: f2gpu.lib.f2_encode_workspace_bytes(ctypes.byref(m), q)
+    assert ws(3 << 30) == ws(1 << 30) > ws((1 << 30) - (1 << 20)) > 0
+    monkeypatch.setenv("F2GPU_ENCODE_CHUNK", "1000003")
+    assert ws(50_000_000) == ws(1_000_003)
+    for bad in ("0", "-5", "x", str((1 << 30) + 1)):   # ignored: the default chunk
+        monkeypatch.setenv("F2GPU_ENCODE_CHUNK", bad)
+        assert ws(3 << 30) == ws(1 << 30)
+
+
 def test_calls_with_bad_host_arguments_enqueue_nothing():
     """Argument errors are returned before any device work (so these run without a GPU)."""
     from paper_2608_20532_amd import f2gpu

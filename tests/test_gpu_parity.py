@@ -753,3 +753,28 @@ def test_fit_deterministic_across_launch_geometries(f2):
         mw, hw = _fit_subset(f2, allw, list(range(3 + extra)))
         outs.append([_ctx_outputs(hw, mw, i) for i in range(3)])
     assert outs[0] == outs[1] == outs[2]
+
+
+@pytest.mark.parametrize("stride,chunk", [(4, 1_000_003), (5, 150_001)])
+def test_encode_chunked_batches_match(f2, monkeypatch, stride, chunk):
+    """Batches above the chunk size (2^30 queries) are encoded chunk by chunk; with the
+    chunk lowered from the host, 3M queries in chunks of about 1M (grouped path, ragged
+    tail) and of 150,001 (gather path; with stride 5 the chunks' x start at odd word
+    offsets) give the words and flags of the one-call encode, which matches the oracle."""
+    import torch
+    wl = synth.fit_workload(3)
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    nq = 3_000_000
+    ctx, x, planted = synth.queries(wl, nq, stride, 0.01, 1.1)
+    ctx_d, x_d = parity.to_dev(ctx), parity.to_dev(x)
+    w0, q0 = f2.encode(model, ctx_d, x_d, stride)
+    monkeypatch.setenv("F2GPU_ENCODE_CHUNK", str(chunk))
+    w1, q1 = f2.encode(model, ctx_d, x_d, stride)
+    monkeypatch.delenv("F2GPU_ENCODE_CHUNK")
+    torch.cuda.synchronize()
+    assert torch.equal(w0, w1) and torch.equal(q0, q1)
+    ref = oracle.fit_batch(wl.rows, wl.row_off, wl.n_bits)
+    sel = np.sort(np.random.default_rng(5).choice(nq, 100_000, replace=False))
+    rw, rq = oracle.encode_batch(ref, ctx[sel], x.reshape(nq, stride)[sel].reshape(-1), stride)
+    assert np.array_equal(w1.cpu().numpy().view(np.uint64)[sel], rw.reshape(-1, 2))
+    assert np.array_equal(q1.cpu().numpy()[sel], rq)
