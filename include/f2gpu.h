@@ -16,9 +16,11 @@
  * ---------------------------------------
  *  - Every pointer argument is DEVICE memory allocated and owned by the
  *    caller unless its name ends in _host.  The library allocates nothing and
- *    keeps no state between calls (beyond a per-device cache of how many
- *    workgroups of the wide-context fit can be resident at once, queried on
- *    first use); concurrent calls need distinct workspaces.
+ *    keeps no state between calls beyond a per-device cache of how many
+ *    workgroups of the wide-context fit can be resident at once (queried on
+ *    first use) and the fixed per-device plan array of f2_fit_batch_noalloc
+ *    (a file-scope device array, part of the loaded library); concurrent
+ *    calls need distinct workspaces.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
  *    device work is enqueued on it; outputs are valid once it has synchronised.
  *  - A negative return value means nothing was enqueued (argument errors that
