@@ -168,7 +168,7 @@ __device__ __forceinline__ CtxDesc readlane_desc(const CtxDesc& v, int t) {
 }
 
 // outputs of an invalid context (one thread)
-__device__ void write_bad_context(const FitArgs& a, const CtxDesc& ds) {
+__device__ __forceinline__ void write_bad_context(const FitArgs& a, const CtxDesc& ds) {
     a.rank[ds.c] = 0;
     a.n_contra[ds.c] = 0;
     a.first_contra[ds.c] = -1;
@@ -382,6 +382,26 @@ __device__ __forceinline__ uint32_t bit_mask(uint64_t w, int b) {
     return static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(dw), b & 31, 1));  // sign of a 1-bit field
 }
 
+// 64 x 64 bit-matrix transpose across a wavefront: lane b holds row b; returned,
+// lane f holds bit f of every row (bit b of the result = bit f of row b).  Six
+// rounds that swap the off-diagonal blocks of size 32, 16, .., 1 with the partner
+// lane (lane xor j).
+template <int J, uint64_t M>
+__device__ __forceinline__ uint64_t transpose_round(uint64_t v, int lane) {
+    const uint32_t plo = static_cast<uint32_t>(__shfl_xor(static_cast<int>(static_cast<uint32_t>(v)), J));
+    const uint32_t phi = static_cast<uint32_t>(__shfl_xor(static_cast<int>(static_cast<uint32_t>(v >> 32)), J));
+    const uint64_t p = (static_cast<uint64_t>(phi) << 32) | plo;
+    return (lane & J) ? ((v & ~M) | ((p & ~M) >> J)) : ((v & M) | ((p & M) << J));
+}
+__device__ __forceinline__ uint64_t transpose64(uint64_t v, int lane) {
+    v = transpose_round<32, 0x00000000ffffffffull>(v, lane);
+    v = transpose_round<16, 0x0000ffff0000ffffull>(v, lane);
+    v = transpose_round<8, 0x00ff00ff00ff00ffull>(v, lane);
+    v = transpose_round<4, 0x0f0f0f0f0f0f0f0full>(v, lane);
+    v = transpose_round<2, 0x3333333333333333ull>(v, lane);
+    return transpose_round<1, 0x5555555555555555ull>(v, lane);
+}
+
 // f ^ (m & d) with m a 32-bit all-ones/zero mask: one v_bitop3 per half
 __device__ __forceinline__ uint64_t xor_and(uint64_t f, uint32_t m, uint64_t d) {
     const uint32_t lo = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(f), m, static_cast<uint32_t>(d), 0x78);
@@ -402,7 +422,7 @@ __device__ __forceinline__ uint64_t xor3(uint64_t a, uint64_t b, uint64_t c) {
 constexpr int kRecWords = 6;  // LDS record: fw feature words, 2 output words, pivot (<= 6 words)
 
 template <int FW>
-__device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec, int16_t* sPos) {
+__device__ __forceinline__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec, int16_t* sPos) {
     constexpr int W = FW + F2_Y_WORDS;
     constexpr int NB = kLongRows / 64;  // blocks of a context in this class
     const int lane = threadIdx.x & 63;
@@ -599,30 +619,29 @@ __device__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds, uint64_t* sRec,
         a.maps[mo + 2 * j] = sl >= 0 ? sRec[sl * kRecWords + FW] : 0ull;
         a.maps[mo + 2 * j + 1] = sl >= 0 ? sRec[sl * kRecWords + FW + 1] : 0ull;
     }
-    // parity-check rows of the free columns (sRec holds the final rows, sPos their records)
+    // parity-check rows of the free columns (sRec holds the final rows, sPos their
+    // records).  Word v of the row of free column fc = 64 w + f holds, at bit b, bit fc
+    // of the basis row of pivot 64 v + b: with lane b holding word w of that basis row
+    // (zero for a free column), a bit-matrix transpose across the wavefront gives lane
+    // f exactly that word; the free lanes then store their rows in ascending order.
     uint64_t* H = a.tables + bo;
-    int slot[FW];
+    if (has_parity_rows(d, rank)) {
+        // (no arrays indexed by the loop counters: where these loops stay rolled,
+        // such an array would live in scratch memory)
+        int base = 0;  // free columns in the words before w
 #pragma unroll
-    for (int w = 0; w < FW; ++w) slot[w] = (64 * w + lane < d) ? sPos[64 * w + lane] : -1;
-    int i = 0;
-    const bool rows = has_parity_rows(d, rank);
-#pragma unroll
-    for (int w = 0; w < FW; ++w) {
-        uint64_t fr = rows ? ~pm[w] & (w == FW - 1 ? tmask : ~0ull) : 0ull;
-        while (fr) {
-            const int fc = 64 * w + ffs64(fr);
-            fr &= fr - 1;
-            uint64_t hv[FW];
+        for (int w = 0; w < FW; ++w) {
+            const int sw = (64 * w + lane < d) ? sPos[64 * w + lane] : -1;
+            const uint64_t fr = ~__ballot(sw >= 0) & (w == FW - 1 ? tmask : ~0ull);
+            const bool mine = (fr >> lane) & 1ull;
+            const int64_t i = base + __popcll(fr & lane_lt);
 #pragma unroll
             for (int v = 0; v < FW; ++v) {
-                const bool has =
-                    slot[v] >= 0 && ((sRec[(slot[v] < 0 ? 0 : slot[v]) * kRecWords + w] >> (fc & 63)) & 1ull);
-                hv[v] = __ballot(has) | (v == w ? (1ull << (fc & 63)) : 0ull);
+                const int sv = (64 * v + lane < d) ? sPos[64 * v + lane] : -1;
+                const uint64_t col = transpose64(sv >= 0 ? sRec[sv * kRecWords + w] : 0ull, lane);
+                if (mine) H[i * FW + v] = col | (v == w ? (1ull << lane) : 0ull);
             }
-#pragma unroll
-            for (int v = 0; v < FW; ++v)
-                if (lane == v) H[static_cast<int64_t>(i) * FW + v] = hv[v];
-            ++i;
+            base += __popcll(fr);
         }
     }
     if (lane == 0) {
