@@ -1080,22 +1080,24 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
         out[fw + 1] = S.rec[j][FW + 1];
         a.pivots[po + k] = j;
     }
-    // parity-check rows of the free columns: wavefront v builds words v, v + NW, ...
+    // parity-check rows of the free columns (word v of the row of free column 64 w + f
+    // holds, at bit b, bit f of word w of the retained row of pivot 64 v + b): per word
+    // pair (w, v), taken by wavefront v mod NW, a bit-matrix transpose of word w of the
+    // retained rows 64 v .. 64 v + 63 (zero for free columns) gives lane f its word
     uint64_t* H = a.tables + bo;
-    int i = 0;
-    const bool rows = has_parity_rows(d, rank);
-    for (int w = 0; w < fw && rows; ++w) {
-        uint64_t fr = ~S.pm[w] & (w == fw - 1 ? tmask : ~0ull);
-        while (fr) {
-            const int f = 64 * w + ffs64(fr);
-            fr &= fr - 1;
+    if (has_parity_rows(d, rank)) {
+        const uint64_t lane_lt = (1ull << lane) - 1;
+        int base = 0;  // free columns in the words before w
+        for (int w = 0; w < fw; ++w) {
+            const uint64_t fr = ~S.pm[w] & (w == fw - 1 ? tmask : ~0ull);
+            const bool mine = (fr >> lane) & 1ull;
+            const int64_t i = base + __popcll(fr & lane_lt);
             for (int v = wave; v < fw; v += NW) {
-                const int p = 64 * v + lane;
-                const bool has = ((S.pm[v] >> lane) & 1ull) && ((S.rec[p][w] >> (f & 63)) & 1ull);
-                const uint64_t hv = __ballot(has) | (v == w ? (1ull << (f & 63)) : 0ull);
-                if (lane == 0) H[static_cast<int64_t>(i) * fw + v] = hv;
+                const bool piv = (S.pm[v] >> lane) & 1ull;
+                const uint64_t col = transpose64(piv ? S.rec[64 * v + lane][w] : 0ull, lane);
+                if (mine) H[i * fw + v] = col | (v == w ? (1ull << lane) : 0ull);
             }
-            ++i;
+            base += __popcll(fr);
         }
     }
     if (tid == 0) {
@@ -1763,23 +1765,25 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
         a.maps[mo + 2 * jj] = present ? row[fw] : 0ull;
         a.maps[mo + 2 * jj + 1] = present ? row[fw + 1] : 0ull;
     }
-    {  // parity-check rows of the free columns: wavefront v builds words v, v + 8, ...
+    {  // parity-check rows of the free columns: per word pair (w, v), taken by wavefront
+       // v mod 8, a bit-matrix transpose of word w of the retained rows of pivots
+       // 64 v .. 64 v + 63 (zero for free columns) gives lane f word v of the row of
+       // free column 64 w + f
         uint64_t* H = a.tables + a.basis_off[c];
-        int i = 0;
-        const bool rows = has_parity_rows(d, rank);
-        for (int w = 0; w < fw && rows; ++w) {
-            uint64_t fr = ~L.pm[w] & (w == fw - 1 ? tmask : ~0ull);
-            while (fr) {
-                const int f = 64 * w + ffs64(fr);
-                fr &= fr - 1;
+        if (has_parity_rows(d, rank)) {
+            const uint64_t lane_lt = (1ull << lane) - 1;
+            int base = 0;  // free columns in the words before w
+            for (int w = 0; w < fw; ++w) {
+                const uint64_t fr = ~L.pm[w] & (w == fw - 1 ? tmask : ~0ull);
+                const bool mine = (fr >> lane) & 1ull;
+                const int64_t i = base + __popcll(fr & lane_lt);
                 for (int v = wave; v < fw; v += kLargeWaves) {
                     const int p = 64 * v + lane;
                     const bool piv = (L.pm[v] >> lane) & 1ull;
-                    const bool has = piv && ((B[static_cast<int64_t>(prio_slot(p, n)) * W + w] >> (f & 63)) & 1ull);
-                    const uint64_t hv = __ballot(has) | (v == w ? (1ull << (f & 63)) : 0ull);
-                    if (lane == 0) H[static_cast<int64_t>(i) * fw + v] = hv;
+                    const uint64_t col = transpose64(piv ? B[static_cast<int64_t>(prio_slot(p, n)) * W + w] : 0ull, lane);
+                    if (mine) H[i * fw + v] = col | (v == w ? (1ull << lane) : 0ull);
                 }
-                ++i;
+                base += __popcll(fr);
             }
         }
     }
