@@ -633,6 +633,7 @@ __device__ __forceinline__ void fit_ctx_reg(const FitArgs& a, const CtxDesc& ds,
         for (int w = 0; w < FW; ++w) {
             const int sw = (64 * w + lane < d) ? sPos[64 * w + lane] : -1;
             const uint64_t fr = ~__ballot(sw >= 0) & (w == FW - 1 ? tmask : ~0ull);
+            if (!fr) continue;  // no free column in this word (full rank: none at all)
             const bool mine = (fr >> lane) & 1ull;
             const int64_t i = base + __popcll(fr & lane_lt);
 #pragma unroll
@@ -1090,6 +1091,7 @@ __device__ __forceinline__ void fit_ctx_piv(const FitArgs& a, const CtxDesc& ds,
         int base = 0;  // free columns in the words before w
         for (int w = 0; w < fw; ++w) {
             const uint64_t fr = ~S.pm[w] & (w == fw - 1 ? tmask : ~0ull);
+            if (!fr) continue;  // no free column in this word
             const bool mine = (fr >> lane) & 1ull;
             const int64_t i = base + __popcll(fr & lane_lt);
             for (int v = wave; v < fw; v += NW) {
@@ -1775,6 +1777,7 @@ __device__ __forceinline__ void fit_ctx_large(const FitArgs& a, const CtxDesc& d
             int base = 0;  // free columns in the words before w
             for (int w = 0; w < fw; ++w) {
                 const uint64_t fr = ~L.pm[w] & (w == fw - 1 ? tmask : ~0ull);
+                if (!fr) continue;  // no free column in this word
                 const bool mine = (fr >> lane) & 1ull;
                 const int64_t i = base + __popcll(fr & lane_lt);
                 for (int v = wave; v < fw; v += kLargeWaves) {
