@@ -734,7 +734,7 @@ constexpr int kPivTabWords = (kPivCap / 2) * kPivRec + kPivTabExtra;
 constexpr int kPivTabMinRank = 32;   // smaller bases reduce as fast record by record
 constexpr int kPivTabMinRows = 512;  // tables are built only with two rounds of rows or more to go
 
-struct PivShared {
+struct alignas(16) PivShared {  // 16-byte aligned: the tables are read 16 bytes at a time
     uint64_t rec[kPivCap][kPivRec];
     uint64_t tabx[kPivTabExtra];  // continues rec (tables)
     int ntab;                     // valid tables (positions [0, 4 ntab)), 0: none
@@ -767,6 +767,24 @@ __device__ __forceinline__ void piv_build_tables(PivShared& S, int d) {
     if (threadIdx.x == 0) S.ntab = nt;
 }
 
+// one table entry of W words from LDS, 16 bytes per read where W is even (the
+// entries then start 16-byte aligned)
+typedef unsigned long long u64x2_t __attribute__((ext_vector_type(2)));
+template <int W>
+__device__ __forceinline__ void load_entry(const uint64_t* e, uint64_t (&v)[W]) {
+    if constexpr (W % 2 == 0) {
+#pragma unroll
+        for (int u = 0; u < W / 2; ++u) {
+            const u64x2_t p = reinterpret_cast<const u64x2_t*>(e)[u];
+            v[2 * u] = p.x;
+            v[2 * u + 1] = p.y;
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < W; ++u) v[u] = e[u];
+    }
+}
+
 // reduce this wavefront's block rows against the retained basis (one pass: the
 // basis is fully reduced).  Positions [0, 4 ntab) by table lookups: the row's own
 // 4 bits at positions 4g .. 4g+3, masked to the pivots, select entry of table g.
@@ -787,19 +805,24 @@ __device__ __forceinline__ void piv_reduce(PivShared& S, int fw, int ntab, uint6
             for (int h = 0; h < 2; ++h) {
                 const uint32_t half = h ? static_cast<uint32_t>(f0[w] >> 32) : static_cast<uint32_t>(f0[w]);
                 const uint32_t pmh = h ? static_cast<uint32_t>(pmw >> 32) : static_cast<uint32_t>(pmw);
-#pragma unroll 1
-                for (int k = 0; k < 8; k += 2) {  // two tables per step, one three-way XOR per word
+#pragma unroll
+                for (int k = 0; k < 8; k += 4) {  // four tables per step: every entry read issued first
                     const int g = 16 * w + 8 * h + k;
                     if (g >= ntab) break;
-                    const uint32_t i0 = __builtin_amdgcn_ubfe(half, 4 * k, 4) & ((pmh >> (4 * k)) & 0xFu);
-                    uint32_t i1 = __builtin_amdgcn_ubfe(half, 4 * k + 4, 4) & ((pmh >> (4 * k + 4)) & 0xFu);
-                    if (g + 1 >= ntab) i1 = 0;  // past the last table: entry 0 of table g (zero)
-                    const uint64_t* e0 = tab + (16 * g + static_cast<int>(i0)) * W;
-                    const uint64_t* e1 = tab + (16 * (g + 1 < ntab ? g + 1 : g) + static_cast<int>(i1)) * W;
+                    uint64_t ev[4][W];
 #pragma unroll
-                    for (int u = 0; u < FW; ++u) f[u] = xor3(f[u], e0[u], e1[u]);
-                    y0 = xor3(y0, e0[FW], e1[FW]);
-                    y1 = xor3(y1, e0[FW + 1], e1[FW + 1]);
+                    for (int q = 0; q < 4; ++q) {
+                        // past the last table: entry 0 of table g (zero)
+                        const bool in = g + q < ntab;
+                        const uint32_t iq = in ? __builtin_amdgcn_ubfe(half, 4 * (k + q), 4) &
+                                                     ((pmh >> (4 * (k + q))) & 0xFu)
+                                               : 0u;
+                        load_entry<W>(tab + (16 * (in ? g + q : g) + static_cast<int>(iq)) * W, ev[q]);
+                    }
+#pragma unroll
+                    for (int u = 0; u < FW; ++u) f[u] = xor3(xor3(f[u], ev[0][u], ev[1][u]), ev[2][u], ev[3][u]);
+                    y0 = xor3(xor3(y0, ev[0][FW], ev[1][FW]), ev[2][FW], ev[3][FW]);
+                    y1 = xor3(xor3(y1, ev[0][FW + 1], ev[1][FW + 1]), ev[2][FW + 1], ev[3][FW + 1]);
                 }
             }
         }
