@@ -2215,41 +2215,41 @@ __global__ __launch_bounds__(kEncThreads) void k_encode(EncArgs e) {
 // context-grouped encode for large batches.  In arbitrary order the lanes of a
 // wavefront gather from as many maps as they hold contexts, one cache line per
 // lane.  A counting sort by bin (2^k consecutive contexts per bin, at most
-// kSortMaxBins bins, or kSortMaxBinsLarge for batches above kDirectMaxQueries
-// (finer bins, an LDS histogram of up to 128 KB), one more bin for out-of-range
-// ids) first groups the
-// queries; the encode then runs over the sorted order, where the lanes of a
-// wavefront share a few contexts and their gathers hit the same lines; a last
-// pass returns the results to query order (up to kDirectMaxQueries queries the
-// results are written straight to their queries instead: scattered writes of a
-// batch that size merge in the last-level cache, larger ones pay for the extra
-// pass with coalesced writes; the sorted passes then store the 16-byte word and
-// an out-of-span bit per result, and the unsort takes the other flags from the
-// context).  The sort uses per-block LDS histograms and scans (no device-wide
-// counters):
-//   count (per block)  ->  column scan (per bin, over blocks)  ->  scatter (bin
-//   scan per block, query -> sorted position)  ->  sorted encode  ->  unsort
+// kSortMaxBins bins, or kSortMaxBinsLarge for batches above kFineBinQueries
+// (finer bins, an LDS histogram of up to 160 KB), one more bin for out-of-range
+// ids) first groups the queries; the encode then runs over the sorted order,
+// where the lanes of a wavefront share a few contexts and their gathers hit the
+// same lines, and writes each result straight to its query.
+//
+// The batch is sorted window by window (bpw consecutive count blocks, about
+// kWindowQueries queries): a query's sorted position stays inside its window.
+// The sorted passes walk the positions in order, so the results they scatter
+// at any time land in the queries of about one window (128 MB of words), which
+// the last-level cache merges before they reach HBM; scattered 16-byte writes
+// over a whole 100M-query batch run at a third of that rate.  The flag bytes
+// are cleared in query order by the scatter; the sorted passes write only the
+// nonzero ones.  The sort uses per-block LDS histograms and scans (no
+// device-wide counters):
+//   count (per block)  ->  column scan (per window and bin, over the window's
+//   blocks)  ->  scatter (bin scan per block, query -> sorted position)  ->
+//   sorted encode  ->  second pass over the positions it leaves
 // ---------------------------------------------------------------------------
 constexpr int kSortThreads = 1024;
 constexpr int kSortMaxBins = 8192;
-constexpr int kSortMaxBinsLarge = 32768;
-constexpr int64_t kDirectMaxQueries = 1 << 22;
+constexpr int kSortMaxBinsLarge = 40000;  // 160,004 bytes of LDS histogram: up to two of 80,000 contexts per bin
+constexpr int64_t kWindowQueries = int64_t{1} << 23;
 
 struct SortArgs {
-    int32_t direct;   // 1: the sorted encode writes each result at its query; 0: through res and the unsort
     int32_t nb;       // bins, the last one for out-of-range context ids
     int32_t bin_shift;  // 2^bin_shift contexts per bin
     int32_t blocks;   // count / scatter blocks
+    int32_t bpw;      // count / scatter blocks per window
     int64_t qc;       // queries per count / scatter block
-    int32_t* hist;    // [blocks][nb], then exclusive offsets within each bin
-    int32_t* total;   // [nb]
+    int32_t* hist;    // [blocks][nb], then exclusive offsets within each bin (of the block's window)
+    int32_t* total;   // [windows][nb]
     int2* perm;       // [nq] sorted position -> (query, context id)
-    int32_t* pos;     // [nq] query -> sorted position
-    Word2* res;       // [nq] result slot -> word
-    uint64_t* oos;    // [ceil(nq / 64)] result slot -> out of span (bit per slot; cleared by the count)
     int32_t regroup;  // 1: each chunk of kRegroupChunk positions regrouped by context (k_enc_regroup)
     int32_t staged;   // 1: k_encode_sorted stages the wavefronts' contexts; 0: every position per lane
-    uint16_t* roff;   // [nq] regrouped position -> its position before, within the chunk (for res)
     uint64_t* rest;   // [ceil(nq / 64)] positions the staged pass left to the second pass (bit per lane)
     int32_t* rest_list;   // [ceil(nq / 64)] the 64-position groups with such positions, in no order
     int32_t* rest_count;  // [1] entries of rest_list (cleared by the count)
@@ -2275,30 +2275,34 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_count(EncArgs e, SortArgs 
         for (int u = 0; u < 4; ++u) atomicAdd(&sBin[query_bin(e, s, c[u])], 1);
     }
     for (; q < q1; q += kSortThreads) atomicAdd(&sBin[query_bin(e, s, e.ctx_id[q])], 1);
-    if (!s.direct)  // the out-of-span bits of the block's slots (a word shared with the next block gets two zero stores)
-        for (int64_t w = (q0 >> 6) + tid; w < ((q1 + 63) >> 6); w += kSortThreads) s.oos[w] = 0;
     if (blockIdx.x == 0 && tid == 0) *s.rest_count = 0;
     __syncthreads();
     int32_t* h = s.hist + static_cast<int64_t>(blockIdx.x) * s.nb;
     for (int b = tid; b < s.nb; b += kSortThreads) h[b] = sBin[b];
 }
 
-// exclusive prefix of each bin over the blocks, in place, and the bin's total.
-// A workgroup takes 64 bins (a lane each) and splits the blocks among its 16
-// wavefronts, so every lane has all of its loads in flight at once.
+// exclusive prefix of each bin over the blocks of its window, in place, and the
+// bin's total in the window.  A workgroup takes 64 bins of one window (a lane
+// each) and splits the window's blocks among its 16 wavefronts, so every lane
+// has all of its loads in flight at once.
 constexpr int kColWaves = 16;
 constexpr int kMaxSortBlocks = 256;
 constexpr int kColPerWave = kMaxSortBlocks / kColWaves;  // blocks per wavefront (at most)
 __global__ __launch_bounds__(64 * kColWaves) void k_enc_colscan(SortArgs s) {
     __shared__ int sPart[kColWaves][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int b = blockIdx.x * 64 + lane;
-    const int per = (s.blocks + kColWaves - 1) / kColWaves;  // <= kColPerWave
-    const int gb = wave * per;
+    const int groups = (s.nb + 63) / 64;  // bin groups per window
+    const int win = blockIdx.x / groups;
+    const int b = (blockIdx.x - win * groups) * 64 + lane;
+    const int bpw = s.bpw > 0 ? s.bpw : s.blocks;  // (no window size: one window of every block)
+    const int wb0 = win * bpw;
+    const int wblocks = s.blocks - wb0 < bpw ? s.blocks - wb0 : bpw;  // <= kMaxSortBlocks
+    const int per = (wblocks + kColWaves - 1) / kColWaves;  // <= kColPerWave
+    const int gb = wb0 + wave * per, ge = wb0 + wblocks;
     int v[kColPerWave];
 #pragma unroll
     for (int k = 0; k < kColPerWave; ++k)
-        v[k] = (b < s.nb && k < per && gb + k < s.blocks) ? s.hist[static_cast<int64_t>(gb + k) * s.nb + b] : 0;
+        v[k] = (b < s.nb && k < per && gb + k < ge) ? s.hist[static_cast<int64_t>(gb + k) * s.nb + b] : 0;
     int sum = 0;
 #pragma unroll
     for (int k = 0; k < kColPerWave; ++k) sum += v[k];
@@ -2313,11 +2317,11 @@ __global__ __launch_bounds__(64 * kColWaves) void k_enc_colscan(SortArgs s) {
     if (b >= s.nb) return;
 #pragma unroll
     for (int k = 0; k < kColPerWave; ++k)
-        if (k < per && gb + k < s.blocks) {
+        if (k < per && gb + k < ge) {
             s.hist[static_cast<int64_t>(gb + k) * s.nb + b] = run;
             run += v[k];
         }
-    if (wave == 0) s.total[b] = total;
+    if (wave == 0) s.total[static_cast<int64_t>(win) * s.nb + b] = total;
 }
 
 // exclusive scan of the bin totals by one workgroup of kSortThreads threads,
@@ -2325,7 +2329,8 @@ __global__ __launch_bounds__(64 * kColWaves) void k_enc_colscan(SortArgs s) {
 // here while the totals are loading).  Up to kBinsPerThread bins per thread the
 // totals stay in registers; more bins (large batches) read them twice.
 constexpr int kBinsPerThread = (kSortMaxBins + 1 + kSortThreads - 1) / kSortThreads;
-__device__ __forceinline__ void bin_offsets(const SortArgs& s, const int32_t* h, int* sBin, int* sWave) {
+__device__ __forceinline__ void bin_offsets(const SortArgs& s, const int32_t* h, const int32_t* total, int* sBin,
+                                            int* sWave) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int per = (s.nb + kSortThreads - 1) / kSortThreads;
     const int b0 = tid * per;
@@ -2334,12 +2339,12 @@ __device__ __forceinline__ void bin_offsets(const SortArgs& s, const int32_t* h,
     int sum = 0;
     if (in_regs) {
 #pragma unroll
-        for (int k = 0; k < kBinsPerThread; ++k) tv[k] = (k < per && b0 + k < s.nb) ? s.total[b0 + k] : 0;
+        for (int k = 0; k < kBinsPerThread; ++k) tv[k] = (k < per && b0 + k < s.nb) ? total[b0 + k] : 0;
 #pragma unroll
         for (int k = 0; k < kBinsPerThread; ++k) sum += tv[k];
     } else {
         for (int k = 0; k < per; ++k)
-            if (b0 + k < s.nb) sum += s.total[b0 + k];
+            if (b0 + k < s.nb) sum += total[b0 + k];
     }
     for (int b = tid; b < s.nb; b += kSortThreads) sBin[b] = h[b];
     int x = sum;
@@ -2362,7 +2367,7 @@ __device__ __forceinline__ void bin_offsets(const SortArgs& s, const int32_t* h,
         for (int k = 0; k < per; ++k)
             if (b0 + k < s.nb) {
                 sBin[b0 + k] += run;
-                run += s.total[b0 + k];
+                run += total[b0 + k];
             }
     }
 }
@@ -2371,16 +2376,31 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_scatter(EncArgs e, SortArg
     extern __shared__ int sBin[];  // [s.nb] (dynamic)
     __shared__ int sWave[kSortThreads / 64];
     const int tid = threadIdx.x;
-    // every block scans the bin totals itself (a few thousand words) instead of a
-    // one-workgroup scan kernel between the column scan and the scatter
-    bin_offsets(s, s.hist + static_cast<int64_t>(blockIdx.x) * s.nb, sBin, sWave);
+    const int win = blockIdx.x / s.bpw;
+    // every block scans its window's bin totals itself (a few thousand words)
+    // instead of a one-workgroup scan kernel between the column scan and the scatter
+    bin_offsets(s, s.hist + static_cast<int64_t>(blockIdx.x) * s.nb, s.total + static_cast<int64_t>(win) * s.nb, sBin,
+                sWave);
     __syncthreads();
     const int64_t q0 = static_cast<int64_t>(blockIdx.x) * s.qc;
     const int64_t q1 = q0 + s.qc < e.nq ? q0 + s.qc : e.nq;
-    auto place = [&](int64_t q, int c, int p) {
-        s.perm[p] = make_int2(static_cast<int>(q), c);
-        if (!s.direct) s.pos[q] = p;
-    };
+    const int64_t base = static_cast<int64_t>(win) * s.bpw * s.qc;  // the window's first query and position
+    // the flag bytes of the block's queries, cleared in order (the sorted passes
+    // write the nonzero ones), 8 at a time from the first 8-byte aligned one
+    {
+        const int mis = static_cast<int>((0 - reinterpret_cast<uintptr_t>(e.qflags)) & 7u);  // qflags + mis is aligned
+        const int64_t a0 = q0 + ((mis - q0) & 7);
+        const int64_t a1 = a0 + (q1 > a0 ? ((q1 - a0) & ~int64_t{7}) : 0);
+        if (a0 < q1) {
+            for (int64_t w = tid; w < ((a1 - a0) >> 3); w += kSortThreads)
+                reinterpret_cast<uint64_t*>(e.qflags + a0)[w] = 0;
+            if (tid < a0 - q0) e.qflags[q0 + tid] = 0;
+            if (tid < q1 - a1) e.qflags[a1 + tid] = 0;
+        } else {
+            for (int64_t q = q0 + tid; q < q1; q += kSortThreads) e.qflags[q] = 0;
+        }
+    }
+    auto place = [&](int64_t q, int c, int p) { s.perm[base + p] = make_int2(static_cast<int>(q), c); };
     int64_t q = q0 + tid;
     for (; q + 3 * kSortThreads < q1; q += 4 * kSortThreads) {
         int c[4], p[4];
@@ -2402,7 +2422,7 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_scatter(EncArgs e, SortArg
 // chunk by chunk (kRegroupChunk positions, in LDS): key = the bin's offset from
 // the chunk's first bin (clamped) and the context's low bits, so within a chunk
 // spanning few bins every context's entries end contiguous.  Entries only move
-// inside their chunk; roff keeps each one's former offset for the result slot.
+// inside their chunk (chunks never straddle a window).
 constexpr int kRegroupThreads = 1024;
 constexpr int kRegroupPer = 4;
 constexpr int kRegroupChunk = kRegroupThreads * kRegroupPer;  // 4096 positions, 12-bit keys
@@ -2411,7 +2431,6 @@ __global__ __launch_bounds__(kRegroupThreads) void k_enc_regroup(EncArgs e, Sort
     __shared__ int sCount[kRegroupChunk];
     __shared__ int sWave[kRegroupThreads / 64];
     __shared__ int2 sEnt[kRegroupChunk];
-    __shared__ uint16_t sOff[kRegroupChunk];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t c0 = static_cast<int64_t>(blockIdx.x) * kRegroupChunk;
     const int n = e.nq - c0 < kRegroupChunk ? static_cast<int>(e.nq - c0) : kRegroupChunk;
@@ -2464,20 +2483,13 @@ __global__ __launch_bounds__(kRegroupThreads) void k_enc_regroup(EncArgs e, Sort
 #pragma unroll
     for (int u = 0; u < kRegroupPer; ++u) {
         const int k = tid + u * kRegroupThreads;
-        if (k < n) {
-            const int dst = sCount[key[u]] + rank[u];
-            sEnt[dst] = ent[u];
-            sOff[dst] = static_cast<uint16_t>(k);
-        }
+        if (k < n) sEnt[sCount[key[u]] + rank[u]] = ent[u];
     }
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < kRegroupPer; ++u) {
         const int k = tid + u * kRegroupThreads;
-        if (k < n) {
-            s.perm[c0 + k] = sEnt[k];
-            if (!s.direct) s.roff[c0 + k] = sOff[k];
-        }
+        if (k < n) s.perm[c0 + k] = sEnt[k];
     }
 }
 
@@ -2748,15 +2760,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
         if (left) s.rest_list[atomicAdd(s.rest_count, 1)] = static_cast<int32_t>(i >> 6);  // a few percent of the groups
     }
     if (!done || !live) return;
-    if (s.direct) {
-        *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
-        e.qflags[qc.x] = static_cast<uint8_t>(fl.x);
-    } else {
-        // the result slot is the position the scatter gave (the regroup moved the entry within its chunk)
-        const int64_t slot = s.regroup ? (i / kRegroupChunk) * kRegroupChunk + s.roff[i] : i;
-        s.res[slot] = out;
-        if (fl.x & F2_Q_OUT_OF_SPAN) atomicOr(&s.oos[slot >> 6], 1ull << (slot & 63));
-    }
+    *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
+    if (fl.x) e.qflags[qc.x] = static_cast<uint8_t>(fl.x);  // the scatter cleared the others
 }
 
 // the second pass over the grouped order: the positions the staged pass left
@@ -2778,7 +2783,6 @@ __device__ __forceinline__ void rest_group(const EncArgs& e, const SortArgs& s, 
     const bool live = i < e.nq && ((bits >> lane) & 1ull);
     if (!__ballot(live)) return;
     const int2 qc = live ? s.perm[i] : make_int2(0, 0);
-    const int64_t slot = (live && !s.direct && s.regroup) ? (i / kRegroupChunk) * kRegroupChunk + s.roff[i] : i;
     const uint64_t* xq = e.x + static_cast<int64_t>(live ? qc.x : 0) * e.stride;
     uint64_t xv[4] = {0, 0, 0, 0};
     if (live) load_x4(e, xq, xv);
@@ -2815,13 +2819,8 @@ __device__ __forceinline__ void rest_group(const EncArgs& e, const SortArgs& s, 
     }
     if (!done) fl = encode_one(e, qc.y, qc.x, out.x, out.y);
     if (!live) return;
-    if (s.direct) {
-        *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
-        e.qflags[qc.x] = fl;
-    } else {
-        s.res[slot] = out;
-        if (fl & F2_Q_OUT_OF_SPAN) atomicOr(&s.oos[slot >> 6], 1ull << (slot & 63));
-    }
+    *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
+    if (fl) e.qflags[qc.x] = fl;
 }
 
 __global__ __launch_bounds__(kEncThreads) void k_encode_rest(EncArgs e, SortArgs s) {
@@ -2845,32 +2844,8 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_lanes(EncArgs e, SortArg
     const int2 qc = s.perm[i];
     Word2 out;
     const uint8_t fl = encode_one(e, qc.y, qc.x, out.x, out.y);
-    if (s.direct) {
-        *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
-        e.qflags[qc.x] = fl;
-    } else {
-        s.res[i] = out;
-        if (fl & F2_Q_OUT_OF_SPAN) atomicOr(&s.oos[i >> 6], 1ull << (i & 63));
-    }
-}
-
-__global__ __launch_bounds__(kEncThreads) void k_enc_unsort(EncArgs e, SortArgs s) {
-    const int64_t q = static_cast<int64_t>(blockIdx.x) * kEncThreads + threadIdx.x;
-    if (q >= e.nq) return;
-    const int64_t i = s.pos[q];
-    const int c = e.ctx_id[q];
-    const Word2 w = s.res[i];
-    const uint64_t o = s.oos[i >> 6];
-    // the flags again from the context (bad, contradictory) and the slot's out-of-span bit
-    uint8_t fl = F2_Q_BAD_CTX;
-    if (c >= 0 && c < e.num_ctx) {
-        const uint32_t cf = e.ctx_flags[c];
-        if (!(cf & kBadCtx))
-            fl = ((cf & F2_CTX_CONTRADICTION) ? F2_Q_CTX_CONTRADICTORY : 0) |
-                 (((o >> (i & 63)) & 1ull) ? F2_Q_OUT_OF_SPAN : 0);
-    }
-    *reinterpret_cast<Word2*>(e.words + 2 * q) = w;
-    e.qflags[q] = fl;
+    *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
+    if (fl) e.qflags[qc.x] = fl;
 }
 
 // ---------------------------------------------------------------------------
@@ -3403,9 +3378,15 @@ unsigned fit_grid(int num_ctx, int cap) { return static_cast<unsigned>(num_ctx <
 // large enough for grouping by context to pay off
 struct EncPlan {
     bool sorted;
+    int windows;
     SortArgs s;
-    size_t off_hist, off_total, off_perm, off_rest, off_rest_list, off_rest_count, off_pos, off_res, off_oos, off_roff, bytes;
+    size_t off_hist, off_total, off_perm, off_rest, off_rest_list, off_rest_count, bytes;
 };
+
+int64_t encode_window();
+
+// batches above this take the fine bins (an LDS histogram of up to 160 KB)
+constexpr int64_t kFineBinQueries = int64_t{1} << 22;
 
 EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     EncPlan p{};
@@ -3416,33 +3397,48 @@ EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     if (!p.sorted) return p;
     const int64_t C = num_ctx > 0 ? num_ctx : 1;
     int shift = 0;
-    // finer bins for large batches (recipe of 100M Zipf queries over 80,000 contexts:
-    // 7.43 ms with 16 contexts per bin, 7.07 with 4); smaller ones keep the small
-    // histogram (a 128 KB one costs its occupancy there)
-    const int maxb = nq > kDirectMaxQueries ? kSortMaxBinsLarge : kSortMaxBins;
+    // finer bins for large batches (100M Zipf queries over 80,000 contexts in
+    // windows of 8M: 6.44 ms with 4 contexts per bin, 6.19 with 2); smaller ones
+    // keep the small histogram (a 160 KB one costs its occupancy there)
+    const int maxb = nq > kFineBinQueries ? kSortMaxBinsLarge : kSortMaxBins;
     while ((C + (int64_t{1} << shift) - 1) >> shift > maxb) ++shift;
     p.s.bin_shift = shift;
     p.s.nb = static_cast<int>((C + (int64_t{1} << shift) - 1) >> shift) + 1;
-    // up to 256 count / scatter blocks of at least 8k queries: enough blocks for the
-    // scatter, few histogram rows to scan (1M queries: 83 us with 8k, 86 with 16k, 88 with 4k)
-    int64_t blocks = (nq + 8191) / 8192;
-    if (blocks > kMaxSortBlocks) blocks = kMaxSortBlocks;
-    const int64_t qc = (nq + blocks - 1) / blocks;
+    // about 256 count / scatter blocks in all (one per compute unit, each with its
+    // histogram), of at least 8k queries: enough blocks for the scatter, few
+    // histogram rows to scan (1M queries: 83 us with 8k, 86 with 16k, 88 with 4k).
+    // Above the window size the blocks form windows of bpw blocks; their size is a
+    // multiple of kRegroupChunk, so no regrouped chunk straddles two windows.
+    const int64_t wq = encode_window();
+    const int64_t windows = (nq + wq - 1) / wq;
+    int64_t qc, bpw;
+    if (windows <= 1) {
+        int64_t blocks = (nq + 8191) / 8192;
+        if (blocks > kMaxSortBlocks) blocks = kMaxSortBlocks;
+        qc = (nq + blocks - 1) / blocks;
+        bpw = blocks;
+    } else {
+        bpw = kMaxSortBlocks / windows > 1 ? kMaxSortBlocks / windows : 1;
+        const int64_t per_window = (nq + windows - 1) / windows;
+        qc = (per_window + bpw - 1) / bpw;
+        qc = (qc + kRegroupChunk - 1) / kRegroupChunk * kRegroupChunk;
+    }
     p.s.qc = qc;
     p.s.blocks = static_cast<int>((nq + qc - 1) / qc);
+    p.s.bpw = static_cast<int>(bpw < p.s.blocks ? bpw : p.s.blocks);
+    p.windows = (p.s.blocks + p.s.bpw - 1) / p.s.bpw;
     size_t o = 0;
     p.off_hist = o;
     o = align256(o + sizeof(int32_t) * static_cast<size_t>(p.s.blocks) * p.s.nb);
     p.off_total = o;
-    o = align256(o + sizeof(int32_t) * p.s.nb);
+    o = align256(o + sizeof(int32_t) * static_cast<size_t>(p.windows) * p.s.nb);
     p.off_perm = o;
     o = align256(o + sizeof(int2) * static_cast<size_t>(nq));
-    p.s.direct = nq <= kDirectMaxQueries;
-    // above 4M queries bins of up to 4 contexts go to the staged pass as they come
-    // (no regroup: 6.95 against 7.09 ms on 100M Zipf queries over 80,000 contexts);
-    // smaller batches regroup when bins hold several contexts and contexts average
-    // 16 queries or more
-    const bool fine = nq > kDirectMaxQueries && shift <= 2;
+    // above kFineBinQueries bins of up to 4 contexts go to the staged pass as they
+    // come (no regroup: 6.95 against 7.09 ms on 100M Zipf queries over 80,000
+    // contexts); smaller batches regroup when bins hold several contexts and
+    // contexts average 16 queries or more
+    const bool fine = nq > kFineBinQueries && shift <= 2;
     p.s.regroup = !fine && shift > 0 && nq >= 16 * C;
     // with one context per bin, fine bins, or after the regroup, a wavefront holds
     // a few contexts and the staged pass applies; otherwise every position goes per lane
@@ -3453,19 +3449,6 @@ EncPlan encode_workspace(int32_t num_ctx, int64_t nq) {
     o = align256(o + sizeof(int32_t) * static_cast<size_t>((nq + 63) / 64));
     p.off_rest_count = o;
     o = align256(o + sizeof(int32_t));
-    p.off_pos = o;
-    p.off_res = o;
-    p.off_roff = o;
-    p.off_oos = o;
-    if (!p.s.direct) {
-        o = align256(o + sizeof(int32_t) * static_cast<size_t>(nq));
-        p.off_res = o;
-        o = align256(o + sizeof(Word2) * static_cast<size_t>(nq));
-        p.off_oos = o;
-        o = align256(o + sizeof(uint64_t) * static_cast<size_t>((nq + 63) / 64));
-        p.off_roff = o;
-        if (p.s.regroup) o = align256(o + sizeof(uint16_t) * static_cast<size_t>(nq));
-    }
     p.bytes = o > 256 ? o : 256;
     return p;
 }
@@ -3499,6 +3482,17 @@ int64_t encode_chunk() {
     char* end = nullptr;
     const long long x = strtoll(v, &end, 10);
     if (*end != '\0' || x < 1 || x > kEncChunk) return kEncChunk;
+    return x;
+}
+
+// queries per sort window: kWindowQueries, or the value of F2GPU_ENCODE_WINDOW
+// (a test hook: several windows at sizes the oracle checks quickly)
+int64_t encode_window() {
+    const char* v = getenv("F2GPU_ENCODE_WINDOW");
+    if (!v || !*v) return kWindowQueries;
+    char* end = nullptr;
+    const long long x = strtoll(v, &end, 10);
+    if (*end != '\0' || x < 1 || x > kEncChunk) return kWindowQueries;
     return x;
 }
 
@@ -3741,16 +3735,13 @@ int encode_range(const f2_model* m, const int32_t* ctx_id, const uint64_t* x, in
     p.s.hist = reinterpret_cast<int32_t*>(ws + p.off_hist);
     p.s.total = reinterpret_cast<int32_t*>(ws + p.off_total);
     p.s.perm = reinterpret_cast<int2*>(ws + p.off_perm);
-    p.s.pos = reinterpret_cast<int32_t*>(ws + p.off_pos);
-    p.s.res = reinterpret_cast<Word2*>(ws + p.off_res);
-    p.s.oos = reinterpret_cast<uint64_t*>(ws + p.off_oos);
-    p.s.roff = reinterpret_cast<uint16_t*>(ws + p.off_roff);
     p.s.rest = reinterpret_cast<uint64_t*>(ws + p.off_rest);
     p.s.rest_list = reinterpret_cast<int32_t*>(ws + p.off_rest_list);
     p.s.rest_count = reinterpret_cast<int32_t*>(ws + p.off_rest_count);
     const size_t bin_lds = sizeof(int) * static_cast<size_t>(p.s.nb);
     hipLaunchKernelGGL(k_enc_count, dim3(p.s.blocks), dim3(kSortThreads), bin_lds, s, e, p.s);
-    hipLaunchKernelGGL(k_enc_colscan, dim3((p.s.nb + 63) / 64), dim3(64 * kColWaves), 0, s, p.s);
+    hipLaunchKernelGGL(k_enc_colscan, dim3(static_cast<unsigned>(p.windows) * ((p.s.nb + 63) / 64)),
+                       dim3(64 * kColWaves), 0, s, p.s);
     hipLaunchKernelGGL(k_enc_scatter, dim3(p.s.blocks), dim3(kSortThreads), bin_lds, s, e, p.s);
     if (p.s.regroup)
         hipLaunchKernelGGL(k_enc_regroup, dim3(static_cast<unsigned>((num_queries + kRegroupChunk - 1) / kRegroupChunk)),
@@ -3762,8 +3753,6 @@ int encode_range(const f2_model* m, const int32_t* ctx_id, const uint64_t* x, in
     } else {
         hipLaunchKernelGGL(k_encode_lanes, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     }
-    if (!p.s.direct)
-        hipLaunchKernelGGL(k_enc_unsort, dim3(static_cast<unsigned>(blocks)), dim3(kEncThreads), 0, s, e, p.s);
     return hipGetLastError() == hipSuccess ? F2_OK : F2_EDEVICE;
 }
 
@@ -3876,6 +3865,7 @@ int f2_group_rows(const int32_t* ctx_id, const uint64_t* rows, int32_t row_strid
     SortArgs cs{};
     cs.nb = kGrpBins;
     cs.blocks = p.blocks;
+    cs.bpw = p.blocks;  // one window: every block
     cs.hist = g.hist;
     cs.total = g.total;
     g.in = nullptr;

@@ -575,15 +575,20 @@ def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
     parity.compare_encode(w3, q3, rw, rq)
 
 
-def test_encode_results_through_the_unsort_with_bad_contexts(f2):
-    """A batch above 4,194,304 queries: the grouped passes keep 16-byte words and an
-    out-of-span bit per result, and the pass back to query order rebuilds the flags from
-    the context; every query is checked, bad contexts and ids out of range included."""
+@pytest.mark.parametrize("window", [None, 1_000_000, 300_007])
+def test_encode_windowed_sort_with_bad_contexts(f2, monkeypatch, window):
+    """A batch above 4,194,304 queries (fine sort bins), sorted as one window or, with the
+    window lowered from the host, window by window (5 windows of 1M, 15 of 300,007 rounded
+    up to whole regroup chunks, a ragged last one); results written straight to their
+    queries and only the nonzero flag bytes over the cleared ones.  Every query is checked,
+    bad contexts and ids out of range included."""
     import torch
     wl, ref, model = _bad_context_model(f2)
     nq, stride = 4_300_000, 2
     ctx, x = _bad_context_queries(wl, nq, stride, 43)
     rw, rq = oracle.encode_batch(ref, ctx, x, stride)
+    if window is not None:
+        monkeypatch.setenv("F2GPU_ENCODE_WINDOW", str(window))
     words, qf = f2.encode(model, parity.to_dev(ctx), parity.to_dev(x), stride)
     torch.cuda.synchronize()
     parity.compare_encode(words, qf, rw, rq)
