@@ -435,7 +435,8 @@ def host_cpu():
 
 def measured_ceilings(stream):
     """Achievable rates from the probe library: a streaming copy (GB/s, bytes read plus
-    written) and a run of independent 32-bit bitwise VALU instructions (T lane ops/s)."""
+    written), a run of independent 32-bit bitwise VALU instructions (T lane ops/s), and
+    scattered 32-byte reads and 16-byte writes (G accesses/s)."""
     import numpy as np
     import torch
     from paper_2608_20532_amd import f2probe
@@ -466,7 +467,16 @@ def measured_ceilings(stream):
     for op, name in ((0, "xor_Tops"), (1, "bitop3_Tops")):
         ms = timed(lambda: f2probe.f2probe_bitops(out, blocks, iters, op, sp), 5)
         res[name] = blocks * 256 * iters * 16 / (ms * 1e-3) / 1e12
-    del src, dst, out
+    # scattered accesses: 32-byte reads over 2 GiB, 16-byte writes over 128 MiB (inside
+    # the last-level cache) and over 2 GiB; G accesses/s
+    sblocks, per = 8192, 16
+    acc = sblocks * 256 * per
+    sout = torch.empty(sblocks * 256, dtype=torch.int64, device=dev)
+    for name, buf, nb, op in (("scatter_read_Gps", src, 8 * words, 0), ("scatter_write_128MiB_Gps", dst, 1 << 27, 1),
+                              ("scatter_write_Gps", dst, 8 * words, 1)):
+        ms = timed(lambda: f2probe.f2probe_scatter(buf, nb, sblocks, per, op, sout, sp), 5)
+        res[name] = acc / (ms * 1e-3) / 1e9
+    del src, dst, out, sout
     torch.cuda.empty_cache()
     return res
 
@@ -644,7 +654,9 @@ def main():
     if not args.no_ceilings:
         ceil = measured_ceilings(stream)
         print(f"[bench] ceilings: copy {ceil['copy_GBps']:.0f} GB/s, xor {ceil['xor_Tops']:.1f} T/s, "
-              f"bitop3 {ceil['bitop3_Tops']:.1f} T/s", file=sys.stderr, flush=True)
+              f"bitop3 {ceil['bitop3_Tops']:.1f} T/s, scattered 32-byte reads {ceil['scatter_read_Gps']:.1f} G/s, "
+              f"16-byte writes {ceil['scatter_write_128MiB_Gps']:.1f} G/s over 128 MiB and "
+              f"{ceil['scatter_write_Gps']:.1f} G/s over 2 GiB", file=sys.stderr, flush=True)
     phases, roof = phases_and_roofline(args.workload, wl, nq, stride, do_fit, fit_ms, enc_ms, rank, ceil)
 
     extras = {}

@@ -2,9 +2,11 @@
  * f2probe.h -- C ABI of the ceiling probes used beside the vendor peaks when a
  * measured rate is turned into a roofline fraction.  They compute nothing of
  * the method: one kernel streams a buffer through HBM (the achievable memory
- * bandwidth), the other issues a long run of independent 32-bit bitwise VALU
+ * bandwidth), one issues a long run of independent 32-bit bitwise VALU
  * operations (the achievable integer issue rate that the blocked elimination
- * of wide contexts is measured against).
+ * of wide contexts is measured against), and one reads or writes at random
+ * positions of a buffer (the achievable rate of scattered accesses, which bounds
+ * the context-grouped encode).
  *
  * Conventions: pointers are DEVICE memory owned by the caller, work is
  * enqueued on `stream` (a hipStream_t passed as void*, NULL = null stream),
@@ -37,6 +39,17 @@ int f2probe_copy(const uint64_t* src, uint64_t* dst, int64_t words, void* stream
  * out holds blocks * 256 uint32 words.  Returns 0, -1 or -3.
  */
 int f2probe_bitops(uint32_t* out, int32_t blocks, int32_t iters, int32_t op, void* stream);
+
+/*
+ * Scattered accesses.  `blocks` workgroups of 256 threads; thread t makes `per`
+ * accesses at slots given by a hash of (t, access index) modulo the number of
+ * slots in the first `bytes` bytes of buf: op 0 reads 32 bytes at a 32-byte slot
+ * (all of them XOR-folded into out[t], so out holds blocks * 256 uint64 words),
+ * op 1 writes 16 bytes at a 16-byte slot (out unused, may be NULL).  Accesses =
+ * blocks * 256 * per.  buf 16-byte aligned, bytes >= 32.  Returns 0, -1 or -3.
+ */
+int f2probe_scatter(uint64_t* buf, int64_t bytes, int32_t blocks, int32_t per, int32_t op, uint64_t* out,
+                    void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,7 +1,8 @@
 // f2probe.hip -- ceiling probes for the roofline figures (gfx950): a streaming
-// non-temporal copy (achievable HBM bandwidth) and a run of independent 32-bit bitwise VALU
-// instructions (achievable integer issue rate).  Nothing here is part of the
-// fit or the encode.
+// non-temporal copy (achievable HBM bandwidth), a run of independent 32-bit bitwise VALU
+// instructions (achievable integer issue rate), and scattered reads and writes at
+// random positions of a buffer (achievable rate of the random accesses that a
+// context-grouped encode makes).  Nothing here is part of the fit or the encode.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -53,9 +54,57 @@ __global__ __launch_bounds__(kThreads) void k_probe_bitops(uint32_t* out, int it
     out[t] = r;
 }
 
+// splitmix64's output function (Steele, Lea and Flood, 2014) as a position hash
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+    z += 0x9e3779b97f4a7c15ull;
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+}
+
+// op 0: each thread reads 32 bytes at `per` random 32-byte slots (XOR-folded, one
+// word stored per thread); op 1: each thread writes 16 bytes at `per` random
+// 16-byte slots
+template <int OP>
+__global__ __launch_bounds__(kThreads) void k_probe_scatter(uint64_t* __restrict__ buf, int64_t slots, int per,
+                                                            uint64_t* __restrict__ out) {
+    const uint64_t t = static_cast<uint64_t>(blockIdx.x) * kThreads + threadIdx.x;
+    uint64_t acc = 0;
+    for (int r = 0; r < per; ++r) {
+        const uint64_t sl = mix64(t * 64 + static_cast<uint64_t>(r)) % static_cast<uint64_t>(slots);
+        if constexpr (OP == 0) {
+            const u32x4* p = reinterpret_cast<const u32x4*>(buf + 4 * sl);
+            const u32x4 a = p[0], b = p[1];
+            acc ^= (static_cast<uint64_t>(a.x ^ b.x) << 32) | (a.y ^ a.z ^ a.w ^ b.y ^ b.z ^ b.w);
+        } else {
+            u32x4 v;
+            v.x = static_cast<uint32_t>(t);
+            v.y = static_cast<uint32_t>(r);
+            v.z = v.w = 0u;
+            *reinterpret_cast<u32x4*>(buf + 2 * sl) = v;
+        }
+    }
+    if constexpr (OP == 0) out[t] = acc;
+}
+
 }  // namespace
 
 extern "C" {
+
+int f2probe_scatter(uint64_t* buf, int64_t bytes, int32_t blocks, int32_t per, int32_t op, uint64_t* out,
+                    void* stream) {
+    if (!buf || bytes < 32 || blocks < 1 || per < 1 || (op != 0 && op != 1) || (op == 0 && !out) ||
+        (reinterpret_cast<uintptr_t>(buf) & 15u))
+        return -1;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (op == 0)
+        hipLaunchKernelGGL(k_probe_scatter<0>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, s, buf, bytes / 32,
+                           per, out);
+    else
+        hipLaunchKernelGGL(k_probe_scatter<1>, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, s, buf, bytes / 16,
+                           per, out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
 
 int f2probe_copy(const uint64_t* src, uint64_t* dst, int64_t words, void* stream) {
     if (words < 0 || (words > 0 && (!src || !dst)) || (words & 1) ||

@@ -1,5 +1,6 @@
-"""Thin ctypes binding of ``libf2probe.so`` (``include/f2probe.h``): the copy and
-integer-issue probes whose measured rates are reported beside the vendor peaks.
+"""Thin ctypes binding of ``libf2probe.so`` (``include/f2probe.h``): the copy,
+integer-issue and scattered-access probes whose measured rates are reported beside
+the vendor peaks.
 Raises on import if the library is not built."""
 from __future__ import annotations
 
@@ -8,7 +9,7 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libf2probe.so")
-EXPORTS = ("f2probe_copy", "f2probe_bitops")
+EXPORTS = ("f2probe_copy", "f2probe_bitops", "f2probe_scatter")
 
 
 def _load():
@@ -20,6 +21,8 @@ def _load():
     L.f2probe_copy.restype = ctypes.c_int
     L.f2probe_bitops.argtypes = [P, i32, i32, i32, P]
     L.f2probe_bitops.restype = ctypes.c_int
+    L.f2probe_scatter.argtypes = [P, i64, i32, i32, i32, P, P]
+    L.f2probe_scatter.restype = ctypes.c_int
     return L
 
 
@@ -36,3 +39,7 @@ def f2probe_copy(src, dst, words: int, stream) -> int:
 
 def f2probe_bitops(out, blocks: int, iters: int, op: int, stream) -> int:
     return int(lib.f2probe_bitops(_ptr(out), int(blocks), int(iters), int(op), int(stream)))
+
+
+def f2probe_scatter(buf, nbytes: int, blocks: int, per: int, op: int, out, stream) -> int:
+    return int(lib.f2probe_scatter(_ptr(buf), int(nbytes), int(blocks), int(per), int(op), _ptr(out), int(stream)))

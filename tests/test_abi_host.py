@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 def test_probe_library_exports_every_declared_symbol():
     from paper_2608_20532_amd import f2probe
     names = declared_functions("f2probe.h", "f2probe_")
-    assert len(names) == 2
+    assert len(names) == 3
     L = ctypes.CDLL(f2probe.LIB_PATH)
     for name in names:
         assert hasattr(L, name), name
@@ -41,6 +41,9 @@ def test_probe_library_exports_every_declared_symbol():
     assert L.f2probe_copy(None, None, 4, None) == -1
     assert L.f2probe_copy(None, None, 0, None) == 0
     assert L.f2probe_bitops(None, 1, 1, 0, None) == -1
+    L.f2probe_scatter.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.c_void_p, ctypes.c_void_p]
+    assert L.f2probe_scatter(None, 1 << 20, 1, 1, 1, None, None) == -1
 
 
 def test_layout_matches_documented_capacities():
