@@ -472,10 +472,10 @@ def test_encode_grouped_path_random_widths(f2, stride):
 
 @pytest.mark.parametrize("stride", [1, 2, 5])
 def test_encode_large_batch_random_widths(f2, stride):
-    """A batch above 4,194,304 queries (x words carried through the sort, nibble-table
-    sorted pass for contexts of 1-127 bits, per-lane pass for wider ones and n = 0)
-    over every width class, with in-span queries, single-bit flips inside and outside
-    the width, junk words and ids out of range; every query compared."""
+    """A batch above 4,194,304 queries (fine sort bins; staged pass for contexts of up to
+    2 feature words, second pass for wider ones and for crowded wavefronts) over every
+    width class, with in-span queries, single-bit flips inside and outside the width,
+    junk words and ids out of range; every query compared."""
     import torch
     rng = np.random.default_rng(100 + stride)
     widths = list(rng.integers(1, 140, size=300)) + [0, 0, 1, 2, 3, 62, 63, 64, 65, 126, 127, 128, 129, 255, 256,
