@@ -145,6 +145,36 @@ def sub_workload(wl, c0, c1):
     return wl.rows[off[0]:off[-1]], off - off[0], wl.n_bits[c0:c1]
 
 
+def oracle_fit_parallel(wl, k, seconds=5.0):
+    """The same oracle fit run as independent context chunks on every usable host core at
+    once (one thread each; the C calls release the interpreter lock): "oracle x N cores"."""
+    import threading
+    import oracle
+    C = wl.num_ctx
+    chunks = [(c0, min(C, c0 + k)) for c0 in range(0, C, k)]
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    done = [0] * n
+    t0 = time.perf_counter()
+
+    def work(tid):
+        j = tid
+        while time.perf_counter() - t0 < seconds:
+            c0, c1 = chunks[j % len(chunks)]
+            rows, off, nb = sub_workload(wl, c0, c1)
+            oracle.fit_batch(rows, off, nb)
+            done[tid] += int(wl.m_rows[c0:c1].sum())
+            j += n
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(n)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    wall = time.perf_counter() - t0
+    return {"value": sum(done) / wall, "unit": "rows/s", "cores": n, "kind": "oracle x N cores",
+            "sample": f"{sum(done)} rows in {wall:.1f} s, chunks of {k} contexts, one thread per core"}
+
+
 def cpu_baseline(wl, ctx, x, stride, nq, do_fit):
     """The oracle (single-threaded C) on a bounded sample of the same workload: context chunks
     in order, repeated, for about ten seconds of fitting; then about five seconds of encoding the
@@ -169,6 +199,7 @@ def cpu_baseline(wl, ctx, x, stride, nq, do_fit):
         out.update(value=rows_fit / t_fit, unit="rows/s",
                    sample=f"oracle fit of {rows_fit} rows: chunks of {k} consecutive contexts of the workload "
                           f"({C} contexts, {wl.total_rows} rows), {t_fit:.1f} s")
+        out["parallel"] = oracle_fit_parallel(wl, k)
     if nq:
         ref, cn = first
         sel = np.nonzero(ctx < cn)[0][:200_000]

@@ -2765,14 +2765,15 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
 }
 
 // the second pass over the grouped order: the positions the staged pass left
-// (their groups in s.rest_list, their lanes in s.rest).  A context holding at
-// least kRestStageLanes of the wavefront's remaining lanes (and up to kEncWideFW
-// feature words) is staged; the other lanes gather per lane.  A fixed grid whose
-// wavefronts take the listed groups in turn: a grid over every position would
-// launch (and allocate the stage for) a workgroup per 256 positions, almost all
-// of them idle (1.2 against 0.42 ms on 100M queries).
-constexpr int kRestStageLanes = 16;
-constexpr int kRestCtxPerWave = 4;  // contexts of a wavefront considered for the stage
+// (their groups in s.rest_list, their lanes in s.rest).  Each context of the
+// group (up to kEncWideFW feature words) is staged in turn, however few of the
+// group's lanes it holds: on 100M Zipf queries that is 0.55 ms against 0.64 with
+// per-lane gathers for contexts of fewer than 16 lanes; wider and bad contexts go
+// per lane.  A fixed grid whose wavefronts take the listed groups in turn: a grid
+// over every position would launch (and allocate the stage for) a workgroup per
+// 256 positions, almost all of them idle (1.2 against 0.42 ms on 100M queries).
+constexpr int kRestStageLanes = 1;
+constexpr int kRestCtxPerWave = 64;  // contexts of a wavefront considered for the stage (all of them)
 constexpr int kRestGrid = 1024;     // workgroups of the listed-group pass
 
 // one wavefront: the lanes of bits among positions i0 .. i0 + 63
