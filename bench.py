@@ -608,6 +608,14 @@ def phases_and_roofline(name, wl, nq, stride, do_fit, fit_ms, enc_ms, rank, ceil
             roof["measured_peak"] = ceil["copy_GBps"]
             roof["measured_peak_unit"] = "GB/s, streaming copy (probe)"
             roof["frac_of_measured_peak"] = phases[dom]["GBps"] / ceil["copy_GBps"]
+            if dom == "encode" and nq >= (1 << 22):
+                # a context-grouped encode reads each query's x at a scattered position and
+                # writes its word at one: one 32-byte read and one 16-byte write per query
+                # at the probes' rates (writes inside the last-level cache: the sort windows)
+                floor_ms = 1e3 * nq * (1.0 / (ceil["scatter_read_Gps"] * 1e9) +
+                                       1.0 / (ceil["scatter_write_128MiB_Gps"] * 1e9))
+                roof["scattered_floor"] = {"ms": floor_ms, "frac": floor_ms / phases[dom]["ms"],
+                                           "per_query": "one scattered 32-byte read, one scattered 16-byte write"}
     if tr:
         roof["kernels"] = tr["kernels"]
         # the bytes the counters saw crossing to the fabric, at the call's measured time
