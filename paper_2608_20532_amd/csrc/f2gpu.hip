@@ -2283,9 +2283,9 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_count(EncArgs e, SortArgs 
 
 // exclusive prefix of each bin over the blocks of its window, in place, and the
 // bin's total in the window.  A workgroup takes 64 bins of one window (a lane
-// each) and splits the window's blocks among its 16 wavefronts, so every lane
+// each) and splits the window's blocks among its kColWaves wavefronts, so every lane
 // has all of its loads in flight at once.
-constexpr int kColWaves = 16;
+constexpr int kColWaves = 8;  // 16: 39 us on 100M queries in 12 windows of ~21 blocks; 8: 32 us
 constexpr int kMaxSortBlocks = 256;
 constexpr int kColPerWave = kMaxSortBlocks / kColWaves;  // blocks per wavefront (at most)
 __global__ __launch_bounds__(64 * kColWaves) void k_enc_colscan(SortArgs s) {
@@ -2774,7 +2774,7 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
 // 256 positions, almost all of them idle (1.2 against 0.42 ms on 100M queries).
 constexpr int kRestStageLanes = 1;
 constexpr int kRestCtxPerWave = 64;  // contexts of a wavefront considered for the stage (all of them)
-constexpr int kRestGrid = 1024;     // workgroups of the listed-group pass
+constexpr int kRestGrid = 2048;     // workgroups of the listed-group pass (100M queries: 0.50 ms; 1,024: 0.54)
 
 // one wavefront: the lanes of bits among positions i0 .. i0 + 63
 __device__ __forceinline__ void rest_group(const EncArgs& e, const SortArgs& s, uint64_t* st, int64_t i0,
