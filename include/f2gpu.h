@@ -185,8 +185,8 @@ int f2_fit_batch_noalloc(const uint64_t* rows, int64_t rows_words, const int64_t
  * each call, may set a smaller chunk (1 .. 2^30; a test hook): the size must be
  * the same when this is called and when f2_encode_batch runs.  Within a chunk,
  * a large batch is grouped by context window by window (about 2^23 queries each);
- * F2GPU_ENCODE_WINDOW (1 .. 2^30, read the same way; a test hook) sets a smaller
- * window, and must likewise be the same for both calls.
+ * F2GPU_ENCODE_WINDOW (1 .. 2^30, raised to 2^16 at least; read the same way; a
+ * test hook) sets a smaller window, and must likewise be the same for both calls.
  */
 size_t f2_encode_workspace_bytes(const f2_model* model_host, int64_t num_queries);
 

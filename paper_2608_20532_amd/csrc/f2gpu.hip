@@ -3487,14 +3487,15 @@ int64_t encode_chunk() {
 }
 
 // queries per sort window: kWindowQueries, or the value of F2GPU_ENCODE_WINDOW
-// (a test hook: several windows at sizes the oracle checks quickly)
+// (a test hook: several windows at sizes the oracle checks quickly), at least
+// 2^16 so that the per-window bin totals stay a small part of the workspace
 int64_t encode_window() {
     const char* v = getenv("F2GPU_ENCODE_WINDOW");
     if (!v || !*v) return kWindowQueries;
     char* end = nullptr;
     const long long x = strtoll(v, &end, 10);
     if (*end != '\0' || x < 1 || x > kEncChunk) return kWindowQueries;
-    return x;
+    return x < (int64_t{1} << 16) ? (int64_t{1} << 16) : x;
 }
 
 FitArgs fit_args(const uint64_t* rows, int64_t rows_words, const int64_t* row_off, const f2_model* m, int32_t* plan) {

@@ -575,13 +575,14 @@ def test_encode_sorted_and_gather_paths_agree_with_bad_contexts(f2):
     parity.compare_encode(w3, q3, rw, rq)
 
 
-@pytest.mark.parametrize("window", [None, 1_000_000, 300_007])
+@pytest.mark.parametrize("window", [None, 1_000_000, 300_007, 65_536])
 def test_encode_windowed_sort_with_bad_contexts(f2, monkeypatch, window):
     """A batch above 4,194,304 queries (fine sort bins), sorted as one window or, with the
     window lowered from the host, window by window (5 windows of 1M, 15 of 300,007 rounded
-    up to whole regroup chunks, a ragged last one); results written straight to their
-    queries and only the nonzero flag bytes over the cleared ones.  Every query is checked,
-    bad contexts and ids out of range included."""
+    up to whole regroup chunks, about 60 of 65,536 with three count blocks each; a ragged
+    last one); results written straight to their queries and only the nonzero flag bytes
+    over the cleared ones.  Every query is checked, bad contexts and ids out of range
+    included."""
     import torch
     wl, ref, model = _bad_context_model(f2)
     nq, stride = 4_300_000, 2
