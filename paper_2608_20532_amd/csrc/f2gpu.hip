@@ -2401,15 +2401,36 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_scatter(EncArgs e, SortArg
         }
     }
     auto place = [&](int64_t q, int c, int p) { s.perm[base + p] = make_int2(static_cast<int>(q), c); };
+    // four queries per thread and step, the next step's ids loaded before this
+    // step's entries are stored and taken (bins computed) after them: the wait
+    // for those loads then leaves the scattered stores in flight (the memory
+    // counter retires in issue order), and the ids of the first step are taken
+    // before the loop, so that no wait at its top covers the stores either
     int64_t q = q0 + tid;
-    for (; q + 3 * kSortThreads < q1; q += 4 * kSortThreads) {
-        int c[4], p[4];
+    if (q + 3 * kSortThreads < q1) {
+        int c[4], b[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) c[u] = e.ctx_id[q + u * kSortThreads];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) p[u] = atomicAdd(&sBin[query_bin(e, s, c[u])], 1);
+        for (int u = 0; u < 4; ++u) b[u] = query_bin(e, s, c[u]);
+        for (;;) {
+            const int64_t qn = q + 4 * kSortThreads;
+            const bool more = qn + 3 * kSortThreads < q1;
+            int cn[4], p[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) place(q + u * kSortThreads, c[u], p[u]);
+            for (int u = 0; u < 4; ++u) cn[u] = e.ctx_id[more ? qn + u * kSortThreads : q];  // (a valid address)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) p[u] = atomicAdd(&sBin[b[u]], 1);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) place(q + u * kSortThreads, c[u], p[u]);
+            q = qn;
+            if (!more) break;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                c[u] = cn[u];
+                b[u] = query_bin(e, s, cn[u]);
+            }
+        }
     }
     for (; q < q1; q += kSortThreads) {
         const int c = e.ctx_id[q];
