@@ -2266,13 +2266,27 @@ __global__ __launch_bounds__(kSortThreads) void k_enc_count(EncArgs e, SortArgs 
     __syncthreads();
     const int64_t q0 = static_cast<int64_t>(blockIdx.x) * s.qc;
     const int64_t q1 = q0 + s.qc < e.nq ? q0 + s.qc : e.nq;
+    // eight ids per thread and step, the next step's loaded before this step's
+    // counts (sixteen loads in flight per thread)
+    constexpr int U = 8;
     int64_t q = q0 + tid;
-    for (; q + 3 * kSortThreads < q1; q += 4 * kSortThreads) {
-        int c[4];
+    if (q + (U - 1) * kSortThreads < q1) {
+        int c[U];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) c[u] = e.ctx_id[q + u * kSortThreads];
+        for (int u = 0; u < U; ++u) c[u] = e.ctx_id[q + u * kSortThreads];
+        for (;;) {
+            const int64_t qn = q + U * kSortThreads;
+            const bool more = qn + (U - 1) * kSortThreads < q1;
+            int cn[U];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) atomicAdd(&sBin[query_bin(e, s, c[u])], 1);
+            for (int u = 0; u < U; ++u) cn[u] = e.ctx_id[more ? qn + u * kSortThreads : q];  // (a valid address)
+#pragma unroll
+            for (int u = 0; u < U; ++u) atomicAdd(&sBin[query_bin(e, s, c[u])], 1);
+            q = qn;
+            if (!more) break;
+#pragma unroll
+            for (int u = 0; u < U; ++u) c[u] = cn[u];
+        }
     }
     for (; q < q1; q += kSortThreads) atomicAdd(&sBin[query_bin(e, s, e.ctx_id[q])], 1);
     if (blockIdx.x == 0 && tid == 0) *s.rest_count = 0;
