@@ -520,6 +520,27 @@ def test_encode_large_batch_random_widths(f2, stride):
     assert (rq & oracle.Q_BAD_CTX).sum() > 10_000 and (rq & oracle.Q_CTX_CONTRADICTORY).any()
 
 
+@pytest.mark.parametrize("stride", [2, 4])
+def test_encode_unaligned_x(f2, stride):
+    """x starting 8 bytes past a 16-byte boundary: the grouped passes take their
+    word-by-word x loads instead of the 16-byte ones (recipe 2's maps, a grouped batch,
+    5% of the queries outside the span); every query compared."""
+    import torch
+    wl = synth.fit_workload(2)
+    ref = parity.oracle_fit_threads(wl.rows, wl.row_off, wl.n_bits)
+    model = parity.gpu_fit(f2, wl.rows, wl.row_off, wl.n_bits)
+    nq = 250_000  # grouped: 196,608 queries or more, four per context
+    ctx, x, _ = synth.queries(wl, nq, stride, 0.05, 0.0)
+    xd = parity.to_dev(np.concatenate([np.zeros(1, np.uint64), x]))[1:]
+    assert xd.data_ptr() % 16 == 8
+    print(f"unaligned-x encode parity: {nq} queries, stride {stride}", flush=True)
+    words, qf = f2.encode(model, parity.to_dev(ctx), xd, stride)
+    torch.cuda.synchronize()
+    rw, rq = parity.oracle_encode_threads(ref, ctx, x, stride)
+    parity.compare_encode(words, qf, rw, rq)
+    assert (rq == 0).sum() > 200_000 and (rq & oracle.Q_OUT_OF_SPAN).sum() > 5_000
+
+
 def _bad_context_model(f2):
     """40 contexts of recipe 2's shape with two malformed ones (1: too wide; 3: a segment
     that is not a whole number of rows), fitted on the GPU; returns (wl, oracle fit, model)."""
