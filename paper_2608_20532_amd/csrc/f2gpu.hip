@@ -2250,7 +2250,7 @@ struct SortArgs {
     int2* perm;       // [nq] sorted position -> (query, context id)
     int32_t regroup;  // 1: each chunk of kRegroupChunk positions regrouped by context (k_enc_regroup)
     int32_t staged;   // 1: k_encode_sorted stages the wavefronts' contexts; 0: every position per lane
-    uint64_t* rest;   // [ceil(nq / 64)] positions the staged pass left to the second pass (bit per lane)
+    uint64_t* rest;   // [ceil(nq / 64)] positions the staged pass left to the second pass (bit per lane; set for the listed groups only)
     int32_t* rest_list;   // [ceil(nq / 64)] the 64-position groups with such positions, in no order
     int32_t* rest_count;  // [1] entries of rest_list (cleared by the count)
 };
@@ -2790,9 +2790,9 @@ __global__ __launch_bounds__(kEncThreads) void k_encode_sorted(EncArgs e, SortAr
         wave_sync();  // the stage is rewritten for the next context
     }
     const uint64_t left = __ballot(!done);  // lanes of further or wider contexts: second pass
-    if ((threadIdx.x & 63) == 0 && i < e.nq) {
+    if (left && (threadIdx.x & 63) == 0) {  // a few percent of the groups (the second pass reads only these)
         s.rest[i >> 6] = left;
-        if (left) s.rest_list[atomicAdd(s.rest_count, 1)] = static_cast<int32_t>(i >> 6);  // a few percent of the groups
+        s.rest_list[atomicAdd(s.rest_count, 1)] = static_cast<int32_t>(i >> 6);
     }
     if (!done || !live) return;
     *reinterpret_cast<Word2*>(e.words + 2 * static_cast<int64_t>(qc.x)) = out;
